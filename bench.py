@@ -1,0 +1,175 @@
+"""Decode-attention benchmark on one MI355X.
+
+One step = one call of the library over one batch of a workload: every cached KV
+byte of every sequence is streamed once (b_kv * sum(seq_lens), App. A.1.2).
+Inputs are seeded synthetic data resident in HBM before timing.  The KV pools are
+replicated `--sets` times in device memory and the calls rotate through the copies,
+so successive calls cannot be served from the 256 MB Infinity Cache.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0   # MI355X HBM3E
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, budget_s):
+    """The CPU oracle as it stands, repeated over the full workload for ~budget_s."""
+    import oracle
+    from paper_2607_09207_amd import accounting as A
+
+    kv = A.call_bytes(w)["kv_unique"]
+    oracle.run(w)   # first call builds/loads the oracle
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.run(w)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    return {
+        "value": round(kv * reps / el / 1e9, 3),
+        "unit": "GB/s",
+        "cores": oracle.max_threads(),
+        "kind": "oracle",
+        "sample": f"{reps} full passes of the {w.name} workload (B={w.batch}, sum(seq_lens)={int(w.seq_lens.sum())}), "
+                  f"fp64, {el:.1f} s wall",
+        "seq_per_s": round(w.batch * reps / el, 1),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="gqa_longtail_bf16")
+    ap.add_argument("--sets", type=int, default=3, help="KV pool copies rotated across calls")
+    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of CPU oracle work (0 = skip)")
+    ap.add_argument("--ranges", type=int, default=0, help="force the number of work ranges (tuning)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (this path needs no "
+              "collectives and shards by sequence or KV head, see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_09207_amd import DecodeAttention, _abi
+    from paper_2607_09207_amd import accounting as A
+    from paper_2607_09207_amd import inputs as I
+
+    _abi.load()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    log(f"generating {args.workload}")
+    w = I.make_workload(args.workload)
+    sets = [I.to_torch(w, dev)]
+    for _ in range(args.sets - 1):
+        s = dict(sets[0])
+        s["k_cache"] = sets[0]["k_cache"].clone()
+        s["v_cache"] = sets[0]["v_cache"].clone()
+        sets.append(s)
+    strides = None if w.layout == "page_head_slot" else w.strides()
+    h = DecodeAttention(w.num_q_heads, w.num_kv_heads, w.head_dim, w.batch, w.max_pages_per_seq, w.q_dtype,
+                        w.kv_dtype, "f32", kv_head_of_q=w.kv_head_of_q, kv_strides=strides,
+                        num_work_ranges=args.ranges)
+    out = torch.empty((w.batch, w.num_q_heads, w.head_dim), dtype=torch.float32, device=dev)
+    ws = h.workspace(dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def call(i, events=None):
+        s = sets[i % len(sets)]
+        h(s["q"], s["k_cache"], s["v_cache"], s["block_table"], s["seq_lens"], k_scale=s["k_scale"],
+          v_scale=s["v_scale"], out=out, workspace=ws, stream=stream, events=events)
+
+    log(f"warmup {args.warmup}")
+    for i in range(args.warmup):
+        call(i)
+    torch.cuda.synchronize()
+
+    log(f"timing {args.steps} steps")
+    # Events bracketing the attention kernel inside each call (recorded by the library
+    # on the same stream), and two around the whole timed region.
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a, b in ev:
+        a.record(stream)
+        b.record(stream)
+    t_all0, t_all1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_all0.record(stream)
+    for i in range(args.steps):
+        call(i, events=ev[i])
+    t_all1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_all0.elapsed_time(t_all1)
+    per_call_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    ms_per_step = total_ms / args.steps
+    kern_ms = float(per_call_ms.mean())
+
+    cb = A.call_bytes(w)
+    kv_bytes = cb["kv_unique"]
+    alg_bytes = A.algorithmic_bytes(w)
+    value = kv_bytes / (ms_per_step * 1e-3) / 1e9
+    achieved = alg_bytes / (kern_ms * 1e-3) / 1e9
+    log(f"ms/step {ms_per_step:.4f}  attention kernel avg {kern_ms:.4f} ms (p10 {np.percentile(per_call_ms, 10):.4f}, "
+        f"p90 {np.percentile(per_call_ms, 90):.4f})  KV {value:.1f} GB/s  seq/s {w.batch / (ms_per_step * 1e-3):.0f}")
+
+    result = {
+        "metric": "decode-attention KV GB/s (fraction of HBM peak) + sequences/s at 1 GPU",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.kv_dtype == "bf16" else ("fp8" if w.kv_dtype == "fp8_e4m3fn" else "f32"),
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "batch": w.batch,
+            "num_q_heads": w.num_q_heads,
+            "num_kv_heads": w.num_kv_heads,
+            "head_dim": w.head_dim,
+            "page_size": w.page_size,
+            "kv_dtype": w.kv_dtype,
+            "sum_seq_lens": int(w.seq_lens.sum()),
+            "kv_bytes_per_step": kv_bytes,
+            "hbm_frac": round(value / PEAK_HBM_GBS, 4),
+            "sequences_per_s": round(w.batch / (ms_per_step * 1e-3), 1),
+            "kv_sets_rotated": len(sets),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBS, 4),
+            "traffic": None,
+        },
+    }
+    if args.cpu_budget > 0:
+        log("cpu baseline (oracle)")
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

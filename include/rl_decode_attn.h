@@ -1,0 +1,152 @@
+/*
+ * rl_decode_attn.h - C ABI of the MI355X (gfx950) decode-attention library.
+ *
+ * Operation.  One decode step of one attention layer for a batch of sequences
+ * that each add one query token, over a paged KV cache: for every sequence b and
+ * query head h,
+ *
+ *     out[b,h,:] = sum_{t < seq_lens[b]} softmax_t(scale * q[b,h,:] . k_t) * v_t
+ *
+ * where k_t, v_t are token t of KV head kv_head_of_q[h] of sequence b.  This is
+ * the computation that dominates the rollout stage the paper schedules: rollout
+ * time is set by autoregressive decode whose long-tail sequences dominate
+ * (Sec. 2.3), decode cost grows with the attended history H_dec and the per-token
+ * KV footprint b_kv (App. A.1.2, rollout model), and GRPO groups of responses
+ * share one prompt (Sec. 2.1).  The paper states no attention formula; the
+ * readings used by this library are:
+ *   - seq_lens[b] counts every cached token including the current one; its K/V
+ *     are already in the cache (the library never writes the cache);
+ *   - seq_lens[b] == 0 yields an all-zero output row;
+ *   - token t of sequence b is slot t % page_size of pool page
+ *     block_table[b * max_pages_per_seq + t / page_size]; entries past
+ *     ceil(seq_lens[b] / page_size) and slots past the end are never read;
+ *   - scale defaults to 1/sqrt(head_dim);
+ *   - fp8 caches use the OCP E4M3FN encoding, and the value of an element is
+ *     decode(byte) * scale[page][kv_head] (one fp32 scale per page and KV head,
+ *     separately for K and V).
+ *
+ * Conventions.
+ *   - Every pointer given to rl_decode_attn_run is DEVICE memory owned by the
+ *     caller and must stay valid until the work queued on `stream` completes.
+ *     The library allocates no device memory and never synchronises the stream.
+ *   - Errors are status codes; nothing throws across this interface.  Argument
+ *     checks that need no device access happen before any launch; a failure
+ *     there launches nothing.
+ *   - A handle owns host memory only; it may be shared by threads, but two calls
+ *     that can overlap (different streams) need different workspaces.
+ */
+#ifndef RL_DECODE_ATTN_H
+#define RL_DECODE_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RLDA_F32 = 0,          /* IEEE binary32 */
+  RLDA_BF16 = 1,         /* bfloat16 (upper half of binary32) */
+  RLDA_FP8_E4M3FN = 2    /* OCP 8-bit E4M3, no infinities, max 448 */
+} rlda_dtype;
+
+typedef enum {
+  RLDA_OK = 0,
+  RLDA_ERR_INVALID_ARG = -1,   /* inconsistent sizes, null or misaligned pointer */
+  RLDA_ERR_UNSUPPORTED = -2,   /* valid request outside the built kernel set */
+  RLDA_ERR_HIP = -3,           /* a HIP runtime call or a launch failed */
+  RLDA_ERR_WORKSPACE = -4,     /* workspace missing or smaller than required */
+  RLDA_ERR_ALLOC = -5          /* host allocation for the handle failed */
+} rlda_status;
+
+typedef struct rlda_handle* rl_decode_attn_t;
+
+/*
+ * Static description of the attention layer and cache.  Supported sets:
+ *   (q, kv, out) = (f32, f32, f32)               head_dim 64 or 128,
+ *                                                group size G = Hq/Hkv with G*head_dim <= 128
+ *   (q, kv, out) = (bf16, bf16 | fp8, f32 | bf16) head_dim 64 or 128, 1 <= G <= 16
+ * page_size must be 16.
+ */
+typedef struct {
+  int32_t num_q_heads;            /* Hq >= 1, at most 256 */
+  int32_t num_kv_heads;           /* Hkv >= 1, divides Hq */
+  int32_t head_dim;               /* d: 64 or 128 */
+  int32_t page_size;              /* P: 16 */
+  int32_t max_batch;              /* largest batch passed to run, 1..8192 */
+  int32_t max_pages_per_seq;      /* block_table row length (elements) */
+  rlda_dtype q_dtype, kv_dtype, out_dtype;
+  const int32_t* kv_head_of_q;    /* HOST array [Hq] copied at create; NULL = h / G.
+                                     Every KV head must receive exactly G query heads. */
+  float softmax_scale;            /* 0 = 1/sqrt(head_dim) */
+  int64_t kv_stride_page;         /* element strides of the K and V caches; d is      */
+  int64_t kv_stride_head;         /* contiguous.  All three 0 = dense layout           */
+  int64_t kv_stride_slot;         /* [page][kv_head][slot][d].  Must keep each row     */
+                                  /* 16-byte aligned; slot stride >= head_dim.         */
+  int32_t num_work_ranges;        /* 0 = fill the GPU (default).  > 0 forces how many
+                                     equal shares the KV work is cut into (tuning and
+                                     tests of the split/merge path); at most 4096.     */
+} rl_decode_attn_config;
+
+/* Validate `cfg` and create a handle (host memory only; no HIP call).
+ * Returns RLDA_ERR_INVALID_ARG / RLDA_ERR_UNSUPPORTED without creating one. */
+rlda_status rl_decode_attn_create(const rl_decode_attn_config* cfg, rl_decode_attn_t* out_handle);
+
+/* Bytes of device workspace a run with this handle needs (host-only). */
+rlda_status rl_decode_attn_workspace_size(rl_decode_attn_t handle, size_t* bytes);
+
+/*
+ * Queue the attention for `batch` sequences on `stream` (a hipStream_t; NULL =
+ * the null stream).  Device arrays, all row-major:
+ *   q            [batch][Hq][d]                   q_dtype
+ *   k_cache,     pool of `num_pages` pages,        kv_dtype, strides from the config
+ *   v_cache
+ *   k_scale,     [num_pages][Hkv] fp32             fp8 caches only, else NULL
+ *   v_scale
+ *   block_table  [batch][max_pages_per_seq] int32  page ids in [0, num_pages)
+ *   seq_lens     [batch] int32                     0 <= L <= max_pages_per_seq*16
+ *   out          [batch][Hq][d]                    out_dtype
+ *   workspace    >= rl_decode_attn_workspace_size bytes, 256-byte aligned, zero-filled
+ *                before its first use (the contract-flag word accumulates); it holds
+ *                partial results between the two kernels of one run.
+ * Pointers q, k_cache, v_cache and out must be 16-byte aligned; with num_pages == 0
+ * (all sequences empty) the cache and scale pointers may be NULL.
+ * Device-side contract violations (a page id outside the pool, a length beyond
+ * the block-table row) never read outside the given arrays: the offending page
+ * or tokens are skipped, the output row is unspecified, and a flag is raised that
+ * rl_decode_attn_read_flags reports.
+ */
+rlda_status rl_decode_attn_run(rl_decode_attn_t handle, int32_t batch, int32_t num_pages, const void* q,
+                               const void* k_cache, const void* v_cache, const float* k_scale,
+                               const float* v_scale, const int32_t* block_table, const int32_t* seq_lens,
+                               void* out, void* workspace, size_t workspace_bytes, void* stream);
+
+/* As rl_decode_attn_run, and records the caller's hipEvent_t `event_begin` /
+ * `event_end` on `stream` immediately before and after the attention kernel (the
+ * kernel that streams the KV cache; a small merge kernel follows it), so callers can
+ * time that kernel alone.  Both events are required. */
+rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t handle, int32_t batch, int32_t num_pages, const void* q,
+                                        const void* k_cache, const void* v_cache, const float* k_scale,
+                                        const float* v_scale, const int32_t* block_table,
+                                        const int32_t* seq_lens, void* out, void* workspace,
+                                        size_t workspace_bytes, void* stream, void* event_begin,
+                                        void* event_end);
+
+/* Flags raised by device-side contract checks since the workspace was zeroed
+ * (bit 0: page id outside [0, num_pages); bit 1: seq_len beyond capacity).
+ * SYNCHRONISES `stream` (waits for queued work, copies 4 bytes to the host). */
+rlda_status rl_decode_attn_read_flags(rl_decode_attn_t handle, const void* workspace, void* stream,
+                                      uint32_t* flags);
+
+/* Destroy a handle; NULL is allowed. */
+rlda_status rl_decode_attn_destroy(rl_decode_attn_t handle);
+
+/* Static description of a status code. */
+const char* rl_decode_attn_strerror(rlda_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RL_DECODE_ATTN_H */

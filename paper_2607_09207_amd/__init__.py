@@ -1,0 +1,162 @@
+"""MI355X (gfx950) decode attention over a paged KV cache.
+
+The computation is the one that dominates the rollout stage of the RL
+post-training loop the paper schedules (Sec. 2.3, App. A.1.2): one query token per
+sequence attending over a paged KV cache with long-tailed lengths and GRPO groups
+that share prompt pages.  All arithmetic runs in the HIP kernels of
+librl_decode_attn.so; this module only marshals torch tensors (device memory and
+the current stream) into the C ABI of include/rl_decode_attn.h.
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Optional
+
+from . import _abi
+
+__all__ = ["DecodeAttention", "decode_attention", "RldaError", "library_path"]
+
+RldaError = _abi.RldaError
+library_path = _abi.LIB_PATH
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t in (torch.float32, "f32"):
+        return _abi.RLDA_F32
+    if t in (torch.bfloat16, "bf16"):
+        return _abi.RLDA_BF16
+    if t in (torch.float8_e4m3fn, "fp8_e4m3fn"):
+        return _abi.RLDA_FP8_E4M3FN
+    raise TypeError(f"unsupported dtype {t}")
+
+
+class DecodeAttention:
+    """A configured decode-attention layer (a library handle).
+
+    k_cache / v_cache passed to __call__ are 4-D tensors of shape
+    [num_pages, num_kv_heads, page_size, head_dim] with head_dim contiguous; any
+    other strides (e.g. a [num_pages, page_size, num_kv_heads, head_dim] buffer
+    viewed with .transpose(1, 2)) are given here as `kv_strides` (elements).
+    """
+
+    def __init__(self, num_q_heads: int, num_kv_heads: int, head_dim: int, max_batch: int,
+                 max_pages_per_seq: int, q_dtype="bf16", kv_dtype="bf16", out_dtype="f32",
+                 kv_head_of_q=None, softmax_scale: float = 0.0, kv_strides=None,
+                 num_work_ranges: int = 0, page_size: int = 16):
+        lib = _abi.load()
+        cfg = _abi.Config()
+        cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim = num_q_heads, num_kv_heads, head_dim
+        cfg.page_size, cfg.max_batch, cfg.max_pages_per_seq = page_size, max_batch, max_pages_per_seq
+        cfg.q_dtype, cfg.kv_dtype, cfg.out_dtype = _dtype_code(q_dtype), _dtype_code(kv_dtype), _dtype_code(out_dtype)
+        self._head_map = None
+        if kv_head_of_q is not None:
+            self._head_map = (ctypes.c_int32 * num_q_heads)(*[int(x) for x in kv_head_of_q])
+            cfg.kv_head_of_q = self._head_map
+        cfg.softmax_scale = float(softmax_scale)
+        if kv_strides is not None:
+            cfg.kv_stride_page, cfg.kv_stride_head, cfg.kv_stride_slot = [int(x) for x in kv_strides]
+        cfg.num_work_ranges = int(num_work_ranges)
+        h = ctypes.c_void_p()
+        _abi.check(lib.rl_decode_attn_create(ctypes.byref(cfg), ctypes.byref(h)), "rl_decode_attn_create")
+        self._lib, self._h, self.config = lib, h, cfg
+        n = ctypes.c_size_t()
+        _abi.check(lib.rl_decode_attn_workspace_size(h, ctypes.byref(n)), "rl_decode_attn_workspace_size")
+        self.workspace_bytes = int(n.value)
+        self._ws = {}
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            self._lib.rl_decode_attn_destroy(h)
+            self._h = None
+
+    def workspace(self, device):
+        """Zero-filled workspace for `device`, allocated once and reused."""
+        torch = _torch()
+        key = str(device)
+        ws = self._ws.get(key)
+        if ws is None:
+            ws = torch.zeros(self.workspace_bytes + 256, dtype=torch.uint8, device=device)
+            self._ws[key] = ws
+        return ws
+
+    @staticmethod
+    def _aligned_ptr(ws) -> int:
+        p = ws.data_ptr()
+        return (p + 255) // 256 * 256
+
+    @staticmethod
+    def _event_handle(ev) -> int:
+        """Raw hipEvent_t of a torch.cuda.Event (created on first record)."""
+        if not ev.cuda_event:
+            ev.record()
+        return ev.cuda_event
+
+    def __call__(self, q, k_cache, v_cache, block_table, seq_lens, k_scale=None, v_scale=None, out=None,
+                 workspace=None, stream=None, num_pages: Optional[int] = None, events=None):
+        """Queue the attention on `stream` (default: the current stream).  With
+        events=(begin, end) (torch.cuda.Event, timing enabled) the two events bracket
+        the attention kernel itself."""
+        torch = _torch()
+        B = int(q.shape[0])
+        cfg = self.config
+        if out is None:
+            odt = torch.float32 if cfg.out_dtype == _abi.RLDA_F32 else torch.bfloat16
+            out = torch.empty((B, cfg.num_q_heads, cfg.head_dim), dtype=odt, device=q.device)
+        ws = workspace if workspace is not None else self.workspace(q.device)
+        if stream is None:
+            stream = torch.cuda.current_stream(q.device).cuda_stream
+        elif hasattr(stream, "cuda_stream"):
+            stream = stream.cuda_stream
+        npages = int(k_cache.shape[0]) if num_pages is None else int(num_pages)
+        ptr = lambda t: None if t is None else t.data_ptr()
+        wp = self._aligned_ptr(ws)
+        args = (self._h, B, npages, ptr(q), ptr(k_cache), ptr(v_cache), ptr(k_scale), ptr(v_scale),
+                ptr(block_table), ptr(seq_lens), ptr(out), wp, ws.numel() - (wp - ws.data_ptr()), stream)
+        if events is None:
+            _abi.check(self._lib.rl_decode_attn_run(*args), "rl_decode_attn_run")
+        else:
+            e0, e1 = (self._event_handle(e) for e in events)
+            _abi.check(self._lib.rl_decode_attn_run_profiled(*args, e0, e1), "rl_decode_attn_run_profiled")
+        return out
+
+    def read_flags(self, workspace=None, device=None, stream=None) -> int:
+        torch = _torch()
+        ws = workspace if workspace is not None else self.workspace(device)
+        if stream is None:
+            stream = torch.cuda.current_stream(ws.device).cuda_stream
+        v = ctypes.c_uint32()
+        _abi.check(self._lib.rl_decode_attn_read_flags(self._h, self._aligned_ptr(ws), stream, ctypes.byref(v)),
+                   "rl_decode_attn_read_flags")
+        return int(v.value)
+
+
+_handles = {}
+
+
+def decode_attention(q, k_cache, v_cache, block_table, seq_lens, *, k_scale=None, v_scale=None,
+                     kv_head_of_q=None, scale: float = 0.0, out=None, out_dtype=None, stream=None):
+    """Functional form: q [B][Hq][d], caches [NP][Hkv][P][d] (d contiguous, any other
+    strides), block_table [B][MP] int32, seq_lens [B] int32, fp8 scales [NP][Hkv]."""
+    torch = _torch()
+    NP, Hkv, P, d = k_cache.shape
+    B, Hq = int(q.shape[0]), int(q.shape[1])
+    if out_dtype is None:
+        out_dtype = out.dtype if out is not None else torch.float32
+    strides = tuple(int(s) for s in k_cache.stride()[:3])
+    if tuple(v_cache.stride()[:3]) != strides or k_cache.stride(3) != 1:
+        raise ValueError("k_cache and v_cache need identical strides with head_dim contiguous")
+    hm = None if kv_head_of_q is None else tuple(int(x) for x in kv_head_of_q)
+    key = (Hq, Hkv, d, P, int(block_table.shape[1]), q.dtype, k_cache.dtype, out_dtype, hm, float(scale), strides)
+    h = _handles.get(key)
+    if h is None or h.config.max_batch < B:
+        h = DecodeAttention(Hq, Hkv, d, max(B, 1), int(block_table.shape[1]), q.dtype, k_cache.dtype, out_dtype,
+                            kv_head_of_q=hm, softmax_scale=scale, kv_strides=strides, page_size=P)
+        _handles[key] = h
+    return h(q, k_cache, v_cache, block_table, seq_lens, k_scale=k_scale, v_scale=v_scale, out=out, stream=stream)

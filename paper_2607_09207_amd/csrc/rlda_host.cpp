@@ -1,0 +1,275 @@
+// Host side of the decode-attention C ABI: argument validation, workspace
+// layout, work-range sizing and the launch.  create/workspace_size/destroy and
+// every argument check of run make no HIP call.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <mutex>
+#include <new>
+
+#include "rl_decode_attn.h"
+#include "rlda_params.h"
+
+struct rlda_handle {
+  rl_decode_attn_config cfg;
+  int32_t group;
+  int64_t stride_page, stride_head, stride_slot;   // elements
+  int32_t ws_ranges;                               // work ranges the workspace is sized for
+  float scale;
+  int16_t q_head[rlda::kMaxQHeads];
+  rlda::KvKind kind;
+  int32_t occupancy;                               // workgroups per CU, queried on first run
+};
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kDefaultWsRanges = 2048;   // covers up to 8 workgroups per CU on 256 CUs
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int elem_bytes(rlda_dtype t) { return t == RLDA_F32 ? 4 : t == RLDA_BF16 ? 2 : 1; }
+
+struct WsLayout {
+  size_t flags, seg_pre, part_ml, part_acc, total;
+};
+
+WsLayout layout_of(const rlda_handle* h) {
+  const rl_decode_attn_config& c = h->cfg;
+  WsLayout w;
+  w.flags = 0;
+  w.seg_pre = align_up(sizeof(uint32_t));
+  w.part_ml = align_up(w.seg_pre + sizeof(int32_t) * ((size_t)c.max_batch + 1));
+  w.part_acc = align_up(w.part_ml + sizeof(float) * 2 * (size_t)h->ws_ranges * h->group * 2);
+  w.total = align_up(w.part_acc + sizeof(float) * 2 * (size_t)h->ws_ranges * h->group * c.head_dim);
+  return w;
+}
+
+// Device properties cached per device id (multiprocessor count).
+std::mutex g_dev_mu;
+int g_cu_count[64];
+
+int cu_count(int dev) {
+  std::lock_guard<std::mutex> lk(g_dev_mu);
+  if (dev < 0 || dev >= 64) return 0;
+  if (g_cu_count[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    g_cu_count[dev] = n;
+  }
+  return g_cu_count[dev];
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+rlda_status rl_decode_attn_create(const rl_decode_attn_config* cfg, rl_decode_attn_t* out_handle) {
+  if (!cfg || !out_handle) return RLDA_ERR_INVALID_ARG;
+  *out_handle = nullptr;
+  const rl_decode_attn_config& c = *cfg;
+  if (c.num_q_heads < 1 || c.num_q_heads > rlda::kMaxQHeads || c.num_kv_heads < 1 ||
+      c.num_q_heads % c.num_kv_heads != 0)
+    return RLDA_ERR_INVALID_ARG;
+  if (c.max_batch < 1 || c.max_batch > rlda::kMaxBatch || c.max_pages_per_seq < 1 ||
+      (int64_t)c.max_pages_per_seq * rlda::kPage > INT32_MAX)
+    return RLDA_ERR_INVALID_ARG;
+  if (c.num_work_ranges < 0 || c.num_work_ranges > rlda::kMaxRanges) return RLDA_ERR_INVALID_ARG;
+  if (!(c.softmax_scale >= 0.f) || isinf(c.softmax_scale)) return RLDA_ERR_INVALID_ARG;
+  if (c.q_dtype < RLDA_F32 || c.q_dtype > RLDA_FP8_E4M3FN || c.kv_dtype < RLDA_F32 ||
+      c.kv_dtype > RLDA_FP8_E4M3FN || c.out_dtype < RLDA_F32 || c.out_dtype > RLDA_FP8_E4M3FN)
+    return RLDA_ERR_INVALID_ARG;
+  if (c.page_size != rlda::kPage) return RLDA_ERR_UNSUPPORTED;
+  if (c.head_dim != 64 && c.head_dim != 128) return RLDA_ERR_UNSUPPORTED;
+  const int G = c.num_q_heads / c.num_kv_heads;
+
+  rlda::KvKind kind;
+  if (c.q_dtype == RLDA_F32 && c.kv_dtype == RLDA_F32 && c.out_dtype == RLDA_F32) {
+    if (G * c.head_dim > 128) return RLDA_ERR_UNSUPPORTED;
+    kind = rlda::KvKind::F32;
+  } else if (c.q_dtype == RLDA_BF16 && (c.kv_dtype == RLDA_BF16 || c.kv_dtype == RLDA_FP8_E4M3FN) &&
+             (c.out_dtype == RLDA_F32 || c.out_dtype == RLDA_BF16)) {
+    if (G > rlda::kMaxGroup) return RLDA_ERR_UNSUPPORTED;
+    kind = c.kv_dtype == RLDA_BF16 ? rlda::KvKind::BF16 : rlda::KvKind::FP8;
+  } else {
+    return RLDA_ERR_UNSUPPORTED;
+  }
+
+  // Strides (elements).  Rows must stay 16-byte aligned and not overlap.
+  int64_t sp = c.kv_stride_page, sh = c.kv_stride_head, ss = c.kv_stride_slot;
+  if (sp == 0 && sh == 0 && ss == 0) {
+    ss = c.head_dim;
+    sh = (int64_t)rlda::kPage * c.head_dim;
+    sp = (int64_t)c.num_kv_heads * sh;
+  }
+  const int eb = elem_bytes(c.kv_dtype);
+  if (sp <= 0 || sh <= 0 || ss < c.head_dim) return RLDA_ERR_INVALID_ARG;
+  if ((sp * eb) % 16 || (sh * eb) % 16 || (ss * eb) % 16) return RLDA_ERR_INVALID_ARG;
+  if ((ss * eb) * (rlda::kPage - 1) + (int64_t)c.head_dim * eb > INT32_MAX) return RLDA_ERR_UNSUPPORTED;
+
+  // Head map: every KV head gets exactly G query heads.
+  int16_t q_head[rlda::kMaxQHeads];
+  int fill[rlda::kMaxQHeads];
+  memset(fill, 0, sizeof fill);
+  for (int h = 0; h < c.num_q_heads; ++h) {
+    const int g = c.kv_head_of_q ? c.kv_head_of_q[h] : h / G;
+    if (g < 0 || g >= c.num_kv_heads || fill[g] >= G) return RLDA_ERR_INVALID_ARG;
+    q_head[g * G + fill[g]++] = (int16_t)h;
+  }
+
+  rlda_handle* hd = new (std::nothrow) rlda_handle;
+  if (!hd) return RLDA_ERR_ALLOC;
+  hd->cfg = c;
+  hd->cfg.kv_head_of_q = nullptr;   // copied into q_head
+  hd->group = G;
+  hd->stride_page = sp;
+  hd->stride_head = sh;
+  hd->stride_slot = ss;
+  hd->ws_ranges = c.num_work_ranges > 0 ? c.num_work_ranges : kDefaultWsRanges;
+  hd->scale = c.softmax_scale > 0.f ? c.softmax_scale : (float)(1.0 / sqrt((double)c.head_dim));
+  memcpy(hd->q_head, q_head, sizeof q_head);
+  hd->kind = kind;
+  hd->occupancy = 0;
+  *out_handle = hd;
+  return RLDA_OK;
+}
+
+rlda_status rl_decode_attn_workspace_size(rl_decode_attn_t h, size_t* bytes) {
+  if (!h || !bytes) return RLDA_ERR_INVALID_ARG;
+  *bytes = layout_of(h).total;
+  return RLDA_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, const void* q, const void* k_cache,
+                     const void* v_cache, const float* k_scale, const float* v_scale, const int32_t* block_table,
+                     const int32_t* seq_lens, void* out, void* workspace, size_t workspace_bytes, void* stream,
+                     void* ev_begin, void* ev_end) {
+  if (!h) return RLDA_ERR_INVALID_ARG;
+  const rl_decode_attn_config& c = h->cfg;
+  if (batch < 0 || batch > c.max_batch || num_pages < 0) return RLDA_ERR_INVALID_ARG;
+  if (batch == 0) return RLDA_OK;
+  if (!q || !block_table || !seq_lens || !out) return RLDA_ERR_INVALID_ARG;
+  // An empty pool (every sequence empty) may come with null cache pointers.
+  if (num_pages > 0 && (!k_cache || !v_cache)) return RLDA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out)) return RLDA_ERR_INVALID_ARG;
+  if (((uintptr_t)block_table & 3u) || ((uintptr_t)seq_lens & 3u)) return RLDA_ERR_INVALID_ARG;
+  const bool fp8 = h->kind == rlda::KvKind::FP8;
+  if (fp8 && num_pages > 0 && (!k_scale || !v_scale || ((uintptr_t)k_scale & 3u) || ((uintptr_t)v_scale & 3u)))
+    return RLDA_ERR_INVALID_ARG;
+  const WsLayout wl = layout_of(h);
+  if (!workspace || ((uintptr_t)workspace % kAlign)) return RLDA_ERR_WORKSPACE;
+  if (workspace_bytes < wl.total) return RLDA_ERR_WORKSPACE;
+
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return RLDA_ERR_HIP;
+  int ranges = c.num_work_ranges;
+  if (ranges == 0) {
+    const int cus = cu_count(dev);
+    int occ = __atomic_load_n(&h->occupancy, __ATOMIC_RELAXED);
+    if (occ == 0) {
+      occ = rlda::occupancy_per_cu(h->kind, c.head_dim, h->group);
+      __atomic_store_n(&h->occupancy, occ, __ATOMIC_RELAXED);
+    }
+    if (cus <= 0 || occ <= 0) return RLDA_ERR_HIP;
+    ranges = cus * occ;
+  }
+  if (ranges > h->ws_ranges) ranges = h->ws_ranges;
+  if (ranges > rlda::kMaxRanges) ranges = rlda::kMaxRanges;
+  // Never more shares than (sequence, KV head, page) units could exist.
+  const int64_t max_units = (int64_t)batch * c.num_kv_heads * c.max_pages_per_seq;
+  if (ranges > max_units) ranges = (int)max_units;
+
+  char* ws = (char*)workspace;
+  rlda::Params p;
+  memset(&p, 0, sizeof p);
+  p.q = q;
+  p.k = k_cache;
+  p.v = v_cache;
+  p.k_scale = k_scale;
+  p.v_scale = v_scale;
+  p.block_table = block_table;
+  p.seq_lens = seq_lens;
+  p.out = out;
+  p.flags = (uint32_t*)(ws + wl.flags);
+  p.seg_pre = (int32_t*)(ws + wl.seg_pre);
+  p.part_ml = (float*)(ws + wl.part_ml);
+  p.part_acc = (float*)(ws + wl.part_acc);
+  const int eb = elem_bytes(c.kv_dtype);
+  p.stride_page = h->stride_page * eb;
+  p.stride_head = h->stride_head * eb;
+  p.stride_slot = (int32_t)(h->stride_slot * eb);
+  p.batch = batch;
+  p.num_pages = num_pages;
+  p.num_q_heads = c.num_q_heads;
+  p.num_kv_heads = c.num_kv_heads;
+  p.group = h->group;
+  p.max_pages = c.max_pages_per_seq;
+  p.nranges = ranges;
+  p.scale_log2 = h->scale * 1.4426950408889634f;
+  p.out_bf16 = c.out_dtype == RLDA_BF16;
+  memcpy(p.q_head, h->q_head, sizeof p.q_head);
+  if (rlda::launch_decode(h->kind, c.head_dim, h->group, p, stream, ev_begin, ev_end) != hipSuccess)
+    return RLDA_ERR_HIP;
+  return RLDA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rlda_status rl_decode_attn_run(rl_decode_attn_t h, int32_t batch, int32_t num_pages, const void* q,
+                               const void* k_cache, const void* v_cache, const float* k_scale,
+                               const float* v_scale, const int32_t* block_table, const int32_t* seq_lens,
+                               void* out, void* workspace, size_t workspace_bytes, void* stream) {
+  return run_impl(h, batch, num_pages, q, k_cache, v_cache, k_scale, v_scale, block_table, seq_lens, out,
+                  workspace, workspace_bytes, stream, nullptr, nullptr);
+}
+
+rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t h, int32_t batch, int32_t num_pages, const void* q,
+                                        const void* k_cache, const void* v_cache, const float* k_scale,
+                                        const float* v_scale, const int32_t* block_table,
+                                        const int32_t* seq_lens, void* out, void* workspace,
+                                        size_t workspace_bytes, void* stream, void* event_begin,
+                                        void* event_end) {
+  if (!event_begin || !event_end) return RLDA_ERR_INVALID_ARG;
+  return run_impl(h, batch, num_pages, q, k_cache, v_cache, k_scale, v_scale, block_table, seq_lens, out,
+                  workspace, workspace_bytes, stream, event_begin, event_end);
+}
+
+rlda_status rl_decode_attn_read_flags(rl_decode_attn_t h, const void* workspace, void* stream, uint32_t* flags) {
+  if (!h || !workspace || !flags) return RLDA_ERR_INVALID_ARG;
+  uint32_t v = 0;
+  if (hipMemcpyAsync(&v, (const char*)workspace + layout_of(h).flags, sizeof v, hipMemcpyDeviceToHost,
+                     (hipStream_t)stream) != hipSuccess)
+    return RLDA_ERR_HIP;
+  if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return RLDA_ERR_HIP;
+  *flags = v;
+  return RLDA_OK;
+}
+
+rlda_status rl_decode_attn_destroy(rl_decode_attn_t h) {
+  delete h;
+  return RLDA_OK;
+}
+
+const char* rl_decode_attn_strerror(rlda_status s) {
+  switch (s) {
+    case RLDA_OK: return "ok";
+    case RLDA_ERR_INVALID_ARG: return "invalid argument";
+    case RLDA_ERR_UNSUPPORTED: return "unsupported configuration";
+    case RLDA_ERR_HIP: return "HIP runtime error";
+    case RLDA_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case RLDA_ERR_ALLOC: return "host allocation failed";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

@@ -1,0 +1,675 @@
+// Decode attention over a paged KV cache for gfx950 (MI355X).
+//
+// One launch does the whole operation (the attention step the paper's rollout
+// model charges through the history term H_dec and the per-token footprint b_kv,
+// App. A.1.2):
+//
+//   1. Work plan.  Every workgroup scans seq_lens into page-count prefix sums in
+//      LDS.  The work is the flattened list of (sequence, KV head, page) units;
+//      workgroup u owns the u-th of nranges equal shares of it.  Long sequences
+//      are therefore cut across many workgroups and short ones packed together:
+//      every workgroup streams the same number of KV pages however long the tail
+//      of the length distribution is (Sec. 2.3 on long-tail decode).
+//   2. Page gather.  Within a share, each maximal run of pages of one
+//      (sequence, KV head) is a "piece"; its pages are split among the 4 waves.
+//      A wave keeps 2-3 pages in flight in registers using buffer loads whose
+//      range check returns zero past a page's last valid token, so masked slots
+//      and pages past the piece cost no memory traffic and never yield NaN.
+//   3. Scores and softmax.  All G query heads that share the KV head are packed
+//      into one 16-row MFMA tile: S^T = K Q^T with v_mfma_f32_16x16x32_bf16; the
+//      online softmax keeps a running max and sum per head in log2 units.
+//   4. PV.  O^T += V^T P^T with v_mfma_f32_16x16x16_bf16: the score tile's output
+//      registers are already the P^T operand, and V's operand is assembled from
+//      4 row loads per lane, so neither operand goes through LDS.
+//   5. Merge.  The 4 waves' (max, sum, O) are merged through LDS.  A piece that
+//      is a whole (sequence, KV head) is normalised and written; otherwise its
+//      unnormalised partial goes to the workspace.
+//   6. A second, small kernel merges the partials of every split (sequence, KV
+//      head) in a fixed order with log-sum-exp weights and writes zero rows for
+//      empty sequences.  The launch boundary is what makes the partials visible
+//      across XCDs; no workgroup waits on another and no device-scope fence is
+//      issued per piece (each such fence writes back and invalidates an XCD's L2).
+// fp8 (OCP E4M3FN) caches are converted exactly to bf16 for the MFMA; the K
+// scale multiplies the scores and the V scale multiplies P.  fp32 caches use a
+// VALU path.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rlda_params.h"
+
+namespace rlda {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+#ifndef RLDA_MFMA_DEPTH
+#define RLDA_MFMA_DEPTH 3                    // pages in flight per wave, MFMA path
+#endif
+constexpr int kChunk = 64;                   // page ids fetched per vector load
+constexpr int kMergeGrid = 1024;             // workgroups of the merge kernel (grid-stride)
+constexpr uint32_t kRsrcWord3 = 0x00020000u; // raw buffer, 32-bit data format
+
+__device__ __forceinline__ float neg_inf() { return -__builtin_huge_valf(); }
+
+// Values equal in every lane, moved to scalar registers so that buffer
+// descriptors and loop bounds built from them stay scalar.
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+__device__ __forceinline__ int64_t uni64(int64_t x) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)x);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)x >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, (int)kRsrcWord3);
+}
+
+template <int BYTES>
+struct RowLoad;
+template <>
+struct RowLoad<16> {
+  typedef u32x4 type;
+  static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  }
+};
+template <>
+struct RowLoad<8> {
+  typedef u32x2 type;
+  static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
+    return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+  }
+};
+template <>
+struct RowLoad<4> {
+  typedef uint32_t type;
+  static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+  }
+};
+
+__device__ __forceinline__ uint32_t word_of(u32x4 v, int i) { return v[i]; }
+__device__ __forceinline__ uint32_t word_of(u32x2 v, int i) { return v[i]; }
+__device__ __forceinline__ uint32_t word_of(uint32_t v, int) { return v; }
+
+// Max / sum over the four 16-lane groups of a wave (lanes l, l^16, l^32, l^48).
+__device__ __forceinline__ float group_max(float x) {
+  x = fmaxf(x, __shfl_xor(x, 16));
+  return fmaxf(x, __shfl_xor(x, 32));
+}
+__device__ __forceinline__ float group_sum(float x) {
+  x += __shfl_xor(x, 16);
+  return x + __shfl_xor(x, 32);
+}
+
+// Two OCP E4M3FN bytes of `w` (bytes 0,1 or, with hi_half, bytes 2,3) as floats.
+__device__ __forceinline__ f32x2 fp8x2_to_f32(uint32_t w, bool hi_half) {
+  return hi_half ? __builtin_amdgcn_cvt_pk_f32_fp8(w, true) : __builtin_amdgcn_cvt_pk_f32_fp8(w, false);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  bf16x2 v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+
+// ---------------------------------------------------------------- MFMA policy
+// Lane l = 16q + i (q = lane group 0..3, i = 0..15).
+// K fragment: lane l holds row (token) i of the page, the 8-element chunks
+//   bf16: chunk 4s+q for k-step s;  fp8: chunks 8(s/2)+2q+(s%2).
+//   Each load instruction of the wave then covers one 64-byte sector per row.
+// V fragment: lane l holds rows 4q..4q+3, elements [D/16*i, D/16*(i+1)).
+// Score tile (D layout of 16x16 MFMA): lane l holds S[token 4q+r][head i].
+// Output tile dt: lane l holds O[head i][d = D/16*(4q+r) + dt].
+template <int D, bool FP8>
+struct Mfma {
+  static constexpr int kD = D;
+  static constexpr bool kFp8 = FP8;
+  static constexpr int KS = D / 32;                  // 16x16x32 k-steps for QK
+  static constexpr int DT = D / 16;                  // output tiles = V elements per row per lane
+  static constexpr int EB = FP8 ? 1 : 2;             // bytes per KV element
+  static constexpr int kEB = EB;
+  static constexpr int kDepth = RLDA_MFMA_DEPTH;
+  static constexpr int KL = FP8 ? D / 64 : D / 32;   // 16-byte K loads per lane
+  static constexpr int VB = DT * EB;                 // V bytes per row per lane
+  typedef typename RowLoad<VB>::type VRow;
+
+  struct Frag {
+    u32x4 k[KL];
+    VRow v[4];
+  };
+
+  f32x4 acc[DT];
+  float m, l;
+  bf16x8 q[KS];
+  int koff[KL], voff[4];
+
+  __device__ __forceinline__ static int chunk_of(int qg, int s) {
+    return FP8 ? 8 * (s >> 1) + 2 * qg + (s & 1) : 4 * s + qg;
+  }
+
+  __device__ __forceinline__ void init(const Params& p, int b, int g, int lane, int32_t ss) {
+    const int i = lane & 15, qg = lane >> 4;
+#pragma unroll
+    for (int t = 0; t < DT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m = neg_inf();
+    l = 0.f;
+    const int G = p.group;
+    const uint16_t* qb = nullptr;
+    if (i < G) qb = (const uint16_t*)p.q + ((int64_t)b * p.num_q_heads + p.q_head[g * G + i]) * D;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      u32x4 w = {0u, 0u, 0u, 0u};
+      if (qb) w = *(const u32x4*)(qb + 8 * chunk_of(qg, s));
+      q[s] = __builtin_bit_cast(bf16x8, w);
+    }
+#pragma unroll
+    for (int s = 0; s < KL; ++s) koff[s] = i * ss + (FP8 ? 64 * s + 16 * qg : 16 * chunk_of(qg, s));
+#pragma unroll
+    for (int r = 0; r < 4; ++r) voff[r] = (4 * qg + r) * ss + i * VB;
+  }
+
+  __device__ __forceinline__ void issue(Frag& f, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv) const {
+#pragma unroll
+    for (int s = 0; s < KL; ++s) f.k[s] = __builtin_amdgcn_raw_buffer_load_b128(rk, koff[s], 0, 0);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) f.v[r] = RowLoad<VB>::load(rv, voff[r]);
+  }
+
+  __device__ __forceinline__ static bf16x8 k_operand(const Frag& f, int s) {
+    if constexpr (!FP8) {
+      return __builtin_bit_cast(bf16x8, f.k[s]);
+    } else {
+      const u32x4 w = f.k[s >> 1];
+      const uint32_t lo = w[2 * (s & 1)], hi = w[2 * (s & 1) + 1];
+      f32x2 a = __builtin_amdgcn_cvt_pk_f32_fp8(lo, false);
+      f32x2 b = __builtin_amdgcn_cvt_pk_f32_fp8(lo, true);
+      f32x2 c = __builtin_amdgcn_cvt_pk_f32_fp8(hi, false);
+      f32x2 d = __builtin_amdgcn_cvt_pk_f32_fp8(hi, true);
+      u32x4 o = {pack_bf16(a[0], a[1]), pack_bf16(b[0], b[1]), pack_bf16(c[0], c[1]), pack_bf16(d[0], d[1])};
+      return __builtin_bit_cast(bf16x8, o);
+    }
+  }
+
+  // Page with index `j` in its sequence; `valid_tokens` tokens of it count.
+  __device__ __forceinline__ void compute(const Frag& f, int lane, int valid_tokens, float kmul, float vmul) {
+    const int qg = lane >> 4;
+    f32x4 sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand(f, s), q[s], sc, 0, 0, 0);
+    float sv[4];
+    float mx = neg_inf();
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      sv[r] = (4 * qg + r < valid_tokens) ? sc[r] * kmul : neg_inf();
+      mx = fmaxf(mx, sv[r]);
+    }
+    mx = group_max(mx);
+    const float mn = fmaxf(m, mx);
+    const float mu = (mn == neg_inf()) ? 0.f : mn;
+    const float alpha = __builtin_amdgcn_exp2f(m - mu);
+    float pr[4];
+    float ps = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      pr[r] = __builtin_amdgcn_exp2f(sv[r] - mu);
+      ps += pr[r];
+    }
+    l = l * alpha + ps;
+    m = mn;
+#pragma unroll
+    for (int t = 0; t < DT; ++t) acc[t] *= alpha;
+    u32x2 pb2 = {pack_bf16(pr[0] * vmul, pr[1] * vmul), pack_bf16(pr[2] * vmul, pr[3] * vmul)};
+    const s16x4 pb = __builtin_bit_cast(s16x4, pb2);
+    if constexpr (!FP8) {
+#pragma unroll
+      for (int t = 0; t < DT; ++t) {
+        const uint32_t w0 = word_of(f.v[0], t >> 1), w1 = word_of(f.v[1], t >> 1);
+        const uint32_t w2 = word_of(f.v[2], t >> 1), w3 = word_of(f.v[3], t >> 1);
+        uint32_t lo, hi;
+        if ((t & 1) == 0) {
+          lo = (w0 & 0xFFFFu) | (w1 << 16);
+          hi = (w2 & 0xFFFFu) | (w3 << 16);
+        } else {
+          lo = (w0 >> 16) | (w1 & 0xFFFF0000u);
+          hi = (w2 >> 16) | (w3 & 0xFFFF0000u);
+        }
+        u32x2 a2 = {lo, hi};
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a2), pb, acc[t], 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < DT / 2; ++u) {   // element pair (2u, 2u+1) of each row
+        f32x2 c[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) c[r] = fp8x2_to_f32(word_of(f.v[r], u >> 1), (u & 1) != 0);
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          u32x2 a2 = {pack_bf16(c[0][e], c[1][e]), pack_bf16(c[2][e], c[3][e])};
+          acc[2 * u + e] =
+              __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a2), pb, acc[2 * u + e], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+  // Write this wave's state in canonical [head][d] form to LDS.
+  __device__ __forceinline__ void to_lds(float (*sacc)[D + 4], float (*sml)[2], int lane) {
+    const int i = lane & 15, qg = lane >> 4;
+    const float lt = group_sum(l);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float* dst = &sacc[i][DT * (4 * qg + r)];
+#pragma unroll
+      for (int t = 0; t < DT; ++t) dst[t] = acc[t][r];
+    }
+    if (qg == 0) {
+      sml[i][0] = m;
+      sml[i][1] = lt;
+    }
+  }
+};
+
+// ---------------------------------------------------------------- VALU policy (fp32 KV)
+// Lane l = 4t + c: token slot t (0..15) of the page, chunk c (0..3) of D/4 values.
+template <int D, int GM>
+struct Valu {
+  static constexpr int kD = D;
+  static constexpr bool kFp8 = false;
+  static constexpr int kEB = 4;
+  static constexpr int kDepth = 2;
+  static constexpr int CW = D / 4;
+  static constexpr int NL = CW / 4;
+  struct Frag {
+    u32x4 k[NL];
+    u32x4 v[NL];
+  };
+  float acc[GM][CW];
+  float qv[GM][CW];
+  float m[GM], l[GM];
+  int off;
+
+  __device__ __forceinline__ void init(const Params& p, int b, int g, int lane, int32_t ss) {
+    const int t = lane >> 2, c = lane & 3;
+    const int G = p.group;
+#pragma unroll
+    for (int h = 0; h < GM; ++h) {
+      m[h] = neg_inf();
+      l[h] = 0.f;
+      const float* qb = nullptr;
+      if (h < G) qb = (const float*)p.q + ((int64_t)b * p.num_q_heads + p.q_head[g * G + h]) * D + c * CW;
+#pragma unroll
+      for (int j = 0; j < CW; ++j) {
+        acc[h][j] = 0.f;
+        qv[h][j] = qb ? qb[j] : 0.f;
+      }
+    }
+    off = t * ss + c * CW * 4;
+  }
+
+  __device__ __forceinline__ void issue(Frag& f, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv) const {
+#pragma unroll
+    for (int s = 0; s < NL; ++s) f.k[s] = __builtin_amdgcn_raw_buffer_load_b128(rk, off + 16 * s, 0, 0);
+#pragma unroll
+    for (int s = 0; s < NL; ++s) f.v[s] = __builtin_amdgcn_raw_buffer_load_b128(rv, off + 16 * s, 0, 0);
+  }
+
+  __device__ __forceinline__ void compute(const Frag& f, int lane, int valid_tokens, float kmul, float) {
+    const int t = lane >> 2;
+    const bool valid = t < valid_tokens;
+#pragma unroll
+    for (int h = 0; h < GM; ++h) {
+      float s = 0.f;
+#pragma unroll
+      for (int j = 0; j < CW; ++j) s += qv[h][j] * __uint_as_float(f.k[j >> 2][j & 3]);
+      s += __shfl_xor(s, 1);
+      s += __shfl_xor(s, 2);
+      s = valid ? s * kmul : neg_inf();
+      float mx = s;
+#pragma unroll
+      for (int o = 4; o < 64; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+      const float mn = fmaxf(m[h], mx);
+      const float mu = (mn == neg_inf()) ? 0.f : mn;
+      const float alpha = __builtin_amdgcn_exp2f(m[h] - mu);
+      const float pr = __builtin_amdgcn_exp2f(s - mu);
+      l[h] = l[h] * alpha + pr;
+      m[h] = mn;
+#pragma unroll
+      for (int j = 0; j < CW; ++j) acc[h][j] = acc[h][j] * alpha + pr * __uint_as_float(f.v[j >> 2][j & 3]);
+    }
+  }
+
+  __device__ __forceinline__ void to_lds(float (*sacc)[D + 4], float (*sml)[2], int lane) {
+    const int c = lane & 3;
+#pragma unroll
+    for (int h = 0; h < GM; ++h) {
+      float lt = l[h];
+#pragma unroll
+      for (int o = 4; o < 64; o <<= 1) lt += __shfl_xor(lt, o);
+#pragma unroll
+      for (int j = 0; j < CW; ++j) {
+        float a = acc[h][j];
+#pragma unroll
+        for (int o = 4; o < 64; o <<= 1) a += __shfl_xor(a, o);
+        acc[h][j] = a;
+      }
+      if (lane < 4) {
+#pragma unroll
+        for (int j = 0; j < CW; ++j) sacc[h][c * CW + j] = acc[h][j];
+      }
+      if (lane == 0) {
+        sml[h][0] = m[h];
+        sml[h][1] = lt;
+      }
+    }
+  }
+};
+
+// ---------------------------------------------------------------- helpers
+
+__device__ __forceinline__ int64_t owner_of(int64_t x, int W, int64_t T) {
+  // Largest u with floor(u*T/W) <= x.
+  return ((x + 1) * (int64_t)W - 1) / T;
+}
+
+template <int D>
+__device__ __forceinline__ void store_out(const Params& p, int b, int qh, int d0, const float* o, float inv) {
+  constexpr int N = D / 16;
+  const int64_t base = ((int64_t)b * p.num_q_heads + qh) * D + d0;
+  if (p.out_bf16) {
+    uint32_t w[N / 2];
+#pragma unroll
+    for (int k = 0; k < N / 2; ++k) w[k] = pack_bf16(o[2 * k] * inv, o[2 * k + 1] * inv);
+    uint32_t* dst = (uint32_t*)((uint16_t*)p.out + base);
+#pragma unroll
+    for (int k = 0; k < N / 2; ++k) dst[k] = w[k];
+  } else {
+    float* dst = (float*)p.out + base;
+#pragma unroll
+    for (int k = 0; k < N; k += 4) {
+      f32x4 v = {o[k] * inv, o[k + 1] * inv, o[k + 2] * inv, o[k + 3] * inv};
+      *(f32x4*)(dst + k) = v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- the kernel
+
+template <class Pol>
+__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(2, 2)))
+void decode_attention_kernel(const Params p) {
+  constexpr int D = Pol::kD;
+  constexpr int DPT = D / 16;   // output elements per thread in the merge
+  __shared__ int32_t s_pre[kMaxBatch + 1];
+  __shared__ float s_acc[kWaves][16][D + 4];
+  __shared__ float s_ml[kWaves][16][2];
+  __shared__ int32_t s_scan[kWaves];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
+  const int u = blockIdx.x, W = p.nranges;
+  const int batch = p.batch, Hkv = p.num_kv_heads, G = p.group;
+  const int cap = p.max_pages * kPage;
+
+  // 1. Page counts per sequence and their prefix sums (identical in every workgroup).
+  {
+    const int per = (batch + kThreads - 1) / kThreads;
+    const int lo = min(tid * per, batch), hi = min(lo + per, batch);
+    int sum = 0, bad = 0;
+    for (int b = lo; b < hi; ++b) {
+      int L = p.seq_lens[b];
+      if (L < 0 || L > cap) bad = 1;
+      L = min(max(L, 0), cap);
+      const int n = (L + kPage - 1) / kPage;
+      s_pre[b + 1] = n;
+      sum += n;
+    }
+    if (bad && u == 0) atomicOr(p.flags, kFlagBadLen);
+    int x = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) s_scan[wave] = x;
+    __syncthreads();
+    int run = x - sum;
+    for (int w = 0; w < wave; ++w) run += s_scan[w];
+    for (int b = lo; b < hi; ++b) {
+      run += s_pre[b + 1];
+      s_pre[b + 1] = run;
+    }
+    if (tid == 0) s_pre[0] = 0;
+    __syncthreads();
+  }
+  const int64_t T = uni64((int64_t)s_pre[batch] * Hkv);
+
+  // 2. The merge kernel reuses the prefix sums.
+  if (u == 0) {
+    for (int b = tid; b <= batch; b += kThreads) p.seg_pre[b] = s_pre[b];
+  }
+
+  // Never more shares than units: every share below Wn is non-empty.
+  const int Wn = (int)min((int64_t)W, T);
+  if (u >= Wn) return;
+
+  // 3. This workgroup's share [r0, r1) of the flattened (sequence, KV head, page) list.
+  const int64_t r0 = (int64_t)u * T / Wn, r1 = (int64_t)(u + 1) * T / Wn;
+  int64_t x = r0;
+  while (x < r1) {
+    const int64_t y = x / Hkv;
+    int lo = 0, hi = batch;   // s_pre[lo] <= y < s_pre[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (s_pre[mid] <= y) lo = mid; else hi = mid;
+    }
+    const int b = uni(lo);
+    const int pre_b = uni(s_pre[b]);
+    const int nb = uni(s_pre[b + 1]) - pre_b;
+    const int64_t off = x - (int64_t)Hkv * pre_b;
+    const int g = (int)(off / nb);
+    const int j0 = (int)(off % nb);
+    const int64_t seg_start = x - j0, seg_end = seg_start + nb;
+    const int64_t pe = min(r1, seg_end);
+    const int j1 = j0 + (int)(pe - x);
+    const bool whole = (j0 == 0) && (pe == seg_end);
+    const int len = min(max(p.seq_lens[b], 0), cap);
+
+    // 3a. This wave's contiguous run of the piece's pages.
+    const int np = j1 - j0;
+    const int per = (np + kWaves - 1) / kWaves;
+    const int ja = min(j0 + wave * per, j1), jb = min(ja + per, j1);
+
+    Pol st;
+    st.init(p, b, g, lane, p.stride_slot);
+    const char* kg = (const char*)p.k + (int64_t)g * p.stride_head;
+    const char* vg = (const char*)p.v + (int64_t)g * p.stride_head;
+    for (int cb = ja; cb < jb; cb += kChunk) {
+      const int cn = min(kChunk, jb - cb);
+      int pid = p.block_table[(int64_t)b * p.max_pages + cb + min(lane, cn - 1)];
+      if ((unsigned)pid >= (unsigned)p.num_pages) {
+        atomicOr(p.flags, kFlagBadPage);
+        pid = -1;
+      }
+      float ksc = 1.f, vsc = 1.f;
+      if constexpr (Pol::kFp8) {
+        ksc = pid >= 0 ? p.k_scale[(int64_t)pid * Hkv + g] : 0.f;
+        vsc = pid >= 0 ? p.v_scale[(int64_t)pid * Hkv + g] : 0.f;
+      }
+      constexpr int kDepth = Pol::kDepth;
+      typename Pol::Frag fr[kDepth];
+      auto issue = [&](typename Pol::Frag& f, int k) {
+        int pk = -1;
+        if (k < cn) pk = __builtin_amdgcn_readlane(pid, k);
+        const int rows = (pk >= 0) ? min(kPage, len - (cb + k) * kPage) : 0;
+        const int64_t po = (pk >= 0) ? (int64_t)pk * p.stride_page : 0;
+        const uint32_t nrec = rows > 0 ? (uint32_t)((rows - 1) * p.stride_slot + D * Pol::kEB) : 0u;
+        st.issue(f, make_rsrc(kg + po, nrec), make_rsrc(vg + po, nrec));
+      };
+      auto compute = [&](const typename Pol::Frag& f, int k) {
+        int valid = 0;
+        float km = p.scale_log2, vm = 1.f;
+        if (k < cn) {
+          const int pk = __builtin_amdgcn_readlane(pid, k);
+          valid = (pk >= 0) ? len - (cb + k) * kPage : 0;
+          if constexpr (Pol::kFp8) {
+            km *= __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ksc), k));
+            vm = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, vsc), k));
+          }
+        }
+        st.compute(f, lane, valid, km, vm);
+      };
+#pragma unroll
+      for (int k = 0; k < kDepth - 1; ++k) issue(fr[k], k);
+      for (int i = 0; i < cn; i += kDepth) {
+#pragma unroll
+        for (int k = 0; k < kDepth; ++k) {
+          issue(fr[(k + kDepth - 1) % kDepth], i + k + kDepth - 1);
+          compute(fr[k], i + k);
+        }
+      }
+    }
+    st.to_lds(s_acc[wave], s_ml[wave], lane);
+    __syncthreads();
+
+    // 3b. Merge the four waves; write the output or this piece's partial.
+    const int h = tid >> 4, d0 = (tid & 15) * DPT;
+    const bool after = (pe == r1) && (pe < seg_end);
+    const int slot = after ? 2 * u + 1 : 2 * u;
+    if (h < G) {
+      float mw[kWaves], M = neg_inf();
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        mw[w] = s_ml[w][h][0];
+        M = fmaxf(M, mw[w]);
+      }
+      float Ls = 0.f, o[DPT];
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) o[e] = 0.f;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const float a = (mw[w] == neg_inf()) ? 0.f : __builtin_amdgcn_exp2f(mw[w] - M);
+        Ls += a * s_ml[w][h][1];
+#pragma unroll
+        for (int e = 0; e < DPT; ++e) o[e] += a * s_acc[w][h][d0 + e];
+      }
+      if (whole) {
+        store_out<D>(p, b, p.q_head[g * G + h], d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
+      } else {
+        float* dst = p.part_acc + ((int64_t)slot * G + h) * D + d0;
+#pragma unroll
+        for (int e = 0; e < DPT; e += 4) *(f32x4*)(dst + e) = f32x4{o[e], o[e + 1], o[e + 2], o[e + 3]};
+        if ((tid & 15) == 0) {
+          p.part_ml[((int64_t)slot * G + h) * 2] = M;
+          p.part_ml[((int64_t)slot * G + h) * 2 + 1] = Ls;
+        }
+      }
+    }
+
+    __syncthreads();
+    x = pe;
+  }
+}
+
+// Split (sequence, KV head) segments: merge their pieces in piece order with
+// log-sum-exp weights.  Empty sequences: zero rows.  One thread per
+// (query head of the group, D/16 output elements); no inter-thread traffic.
+template <int D>
+__global__ __launch_bounds__(kThreads) void merge_pieces_kernel(const Params p) {
+  constexpr int DPT = D / 16;
+  const int tid = threadIdx.x;
+  const int h = tid >> 4, d0 = (tid & 15) * DPT;
+  const int batch = p.batch, Hkv = p.num_kv_heads, G = p.group;
+  if (h >= G) return;
+  const int64_t T = (int64_t)p.seg_pre[batch] * Hkv;
+  const int Wn = (int)min((int64_t)p.nranges, T);
+  const int nseg = batch * Hkv;
+  for (int sgi = blockIdx.x; sgi < nseg; sgi += gridDim.x) {
+    const int b = sgi / Hkv, g = sgi - b * Hkv;
+    const int pre_b = p.seg_pre[b], nb = p.seg_pre[b + 1] - pre_b;
+    const int qh = p.q_head[g * G + h];
+    float o[DPT];
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) o[e] = 0.f;
+    if (nb == 0) {
+      store_out<D>(p, b, qh, d0, o, 0.f);
+      continue;
+    }
+    const int64_t seg_start = (int64_t)Hkv * pre_b + (int64_t)g * nb, seg_end = seg_start + nb;
+    const int64_t u_first = owner_of(seg_start, Wn, T), u_last = owner_of(seg_end - 1, Wn, T);
+    if (u_first == u_last) continue;   // written whole by the attention kernel
+    // piece of workgroup k: slot 2k+1 when it continues past k's share, else slot 2k
+    float M = neg_inf();
+    for (int64_t k = u_first; k <= u_last; ++k) {
+      const int64_t sl = (k < u_last) ? 2 * k + 1 : 2 * k;
+      M = fmaxf(M, p.part_ml[(sl * G + h) * 2]);
+    }
+    float Ls = 0.f;
+    for (int64_t k = u_first; k <= u_last; ++k) {
+      const int64_t sl = (k < u_last) ? 2 * k + 1 : 2 * k;
+      const float mk = p.part_ml[(sl * G + h) * 2];
+      const float a = (mk == neg_inf()) ? 0.f : __builtin_amdgcn_exp2f(mk - M);
+      Ls += a * p.part_ml[(sl * G + h) * 2 + 1];
+      const f32x4* src = (const f32x4*)(p.part_acc + (sl * G + h) * D + d0);
+#pragma unroll
+      for (int e = 0; e < DPT / 4; ++e) {
+        const f32x4 v = src[e];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) o[4 * e + c] += a * v[c];
+      }
+    }
+    store_out<D>(p, b, qh, d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
+  }
+}
+
+template <class Pol>
+int launch(const Params& p, void* stream, void* ev_begin, void* ev_end) {
+  hipStream_t st = (hipStream_t)stream;
+  if (ev_begin && hipEventRecord((hipEvent_t)ev_begin, st) != hipSuccess) return -1;
+  hipLaunchKernelGGL(decode_attention_kernel<Pol>, dim3(p.nranges), dim3(kThreads), 0, st, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return (int)e;
+  if (ev_end && hipEventRecord((hipEvent_t)ev_end, st) != hipSuccess) return -1;
+  const int nseg = p.batch * p.num_kv_heads;
+  const int grid = nseg < kMergeGrid ? nseg : kMergeGrid;
+  hipLaunchKernelGGL(merge_pieces_kernel<Pol::kD>, dim3(grid), dim3(kThreads), 0, st, p);
+  return (int)hipGetLastError();
+}
+
+template <class Pol>
+int occupancy() {
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_attention_kernel<Pol>, kThreads, 0) != hipSuccess)
+    return 0;
+  return n;
+}
+
+}  // namespace
+
+#define RLDA_DISPATCH(FN, ...)                                                  \
+  switch (kind) {                                                               \
+    case KvKind::BF16:                                                          \
+      return head_dim == 128 ? FN<Mfma<128, false>>(__VA_ARGS__)                \
+                             : FN<Mfma<64, false>>(__VA_ARGS__);                \
+    case KvKind::FP8:                                                           \
+      return head_dim == 128 ? FN<Mfma<128, true>>(__VA_ARGS__)                 \
+                             : FN<Mfma<64, true>>(__VA_ARGS__);                 \
+    case KvKind::F32:                                                           \
+      if (head_dim == 128) return FN<Valu<128, 1>>(__VA_ARGS__);                \
+      return group == 1 ? FN<Valu<64, 1>>(__VA_ARGS__) : FN<Valu<64, 2>>(__VA_ARGS__); \
+  }                                                                             \
+  return -1;
+
+int launch_decode(KvKind kind, int head_dim, int group, const Params& p, void* stream, void* ev_begin,
+                  void* ev_end) {
+  RLDA_DISPATCH(launch, p, stream, ev_begin, ev_end)
+}
+
+int occupancy_per_cu(KvKind kind, int head_dim, int group) { RLDA_DISPATCH(occupancy, ) }
+
+}  // namespace rlda

@@ -1,0 +1,55 @@
+// Internal launch parameters shared by the host entry points and the kernels.
+#pragma once
+#include <stdint.h>
+
+namespace rlda {
+
+constexpr int kPage = 16;          // tokens per KV page
+constexpr int kWaves = 4;          // waves per workgroup
+constexpr int kThreads = 64 * kWaves;
+constexpr int kMaxQHeads = 256;
+constexpr int kMaxBatch = 8192;
+constexpr int kMaxRanges = 4096;   // upper bound on work ranges (= workgroups)
+constexpr int kMaxGroup = 16;      // query heads per KV head packed in one MFMA tile
+
+// Bits of the device-side contract flag word.
+constexpr uint32_t kFlagBadPage = 1u;
+constexpr uint32_t kFlagBadLen = 2u;
+
+struct Params {
+  const void* q;               // [batch][Hq][D]
+  const void* k;               // KV pools (byte addressed through the strides)
+  const void* v;
+  const float* k_scale;        // [num_pages][Hkv] (fp8 only)
+  const float* v_scale;
+  const int32_t* block_table;  // [batch][max_pages]
+  const int32_t* seq_lens;     // [batch]
+  void* out;                   // [batch][Hq][D]
+  float* part_acc;             // [2 * nranges][G][D]  unnormalised partial outputs
+  float* part_ml;              // [2 * nranges][G][2]  (running max in log2 units, sum)
+  int32_t* seg_pre;            // [batch + 1] page-count prefix sums, for the merge kernel
+  uint32_t* flags;             // contract-violation bits
+  int64_t stride_page;         // bytes
+  int64_t stride_head;         // bytes
+  int32_t stride_slot;         // bytes
+  int32_t batch;
+  int32_t num_pages;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t group;               // G = Hq / Hkv
+  int32_t max_pages;           // block-table row length
+  int32_t nranges;             // workgroups = equal shares of the flattened work
+  float scale_log2;            // softmax scale * log2(e)
+  int32_t out_bf16;            // 0: fp32 output, 1: bf16 output
+  int16_t q_head[kMaxQHeads];  // q_head[g * G + i] = i-th query head of KV head g
+};
+
+enum class KvKind { F32, BF16, FP8 };
+
+// Kernel launchers (rlda_kernels.hip).  Return hipSuccess or the launch error.
+// The attention kernel is bracketed by ev_begin / ev_end when they are non-null.
+int launch_decode(KvKind kind, int head_dim, int group, const Params& p, void* stream, void* ev_begin,
+                  void* ev_end);
+int occupancy_per_cu(KvKind kind, int head_dim, int group);
+
+}  // namespace rlda

@@ -400,3 +400,35 @@ def permute_pages(w: Workload, seed: int = 99) -> Workload:
     vs = None if w.v_scale is None else np.ascontiguousarray(w.v_scale[old_of_new])
     bt = np.where(w.block_table >= 0, new_of_old[np.maximum(w.block_table, 0)], -1).astype(np.int32)
     return dataclasses.replace(w, k_cache=k, v_cache=v, k_scale=ks, v_scale=vs, block_table=bt)
+
+
+def to_torch(w: Workload, device="cuda"):
+    """Device tensors for a workload: q, k_cache, v_cache as [NP][Hkv][P][d] views
+    (strided when the pool is laid out [NP][P][Hkv][d]), scales, block_table, seq_lens."""
+    import torch
+
+    def dev(a, dt=None):
+        t = torch.from_numpy(np.ascontiguousarray(a))
+        if dt is not None:
+            t = t.view(dt)
+        return t.to(device)
+
+    def raw(a, kind):
+        if kind == "bf16":
+            return dev(a.view(np.int16), torch.bfloat16)
+        if kind == "fp8_e4m3fn":
+            return dev(a, torch.float8_e4m3fn)
+        return dev(a)
+
+    k, v = raw(w.k_cache, w.kv_dtype), raw(w.v_cache, w.kv_dtype)
+    if w.layout == "page_slot_head":
+        k, v = k.transpose(1, 2), v.transpose(1, 2)
+    return {
+        "q": raw(w.q, w.q_dtype),
+        "k_cache": k,
+        "v_cache": v,
+        "k_scale": None if w.k_scale is None else dev(w.k_scale),
+        "v_scale": None if w.v_scale is None else dev(w.v_scale),
+        "block_table": dev(w.block_table),
+        "seq_lens": dev(w.seq_lens),
+    }

@@ -1,0 +1,152 @@
+"""C ABI checks that need no GPU: exports, config validation, argument errors.
+
+create / workspace_size / destroy / strerror make no HIP call, and run() rejects
+bad arguments before touching the device, so all of this runs on the CPU.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_09207_amd import _abi
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_abi.LIB_PATH):
+        from paper_2607_09207_amd import build
+        build.build()
+    return _abi.load()
+
+
+def declared_functions():
+    txt = open(os.path.join(ROOT, "include", "rl_decode_attn.h")).read()
+    return sorted(set(re.findall(r"^(?:rlda_status|const char\*)\s+(rl_decode_attn_\w+)\s*\(", txt, re.M)))
+
+
+def test_every_declared_function_is_exported(lib):
+    names = declared_functions()
+    assert set(names) == set(_abi.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def cfg(**kw):
+    c = _abi.Config()
+    base = dict(num_q_heads=28, num_kv_heads=4, head_dim=128, page_size=16, max_batch=64, max_pages_per_seq=1024,
+                q_dtype=_abi.RLDA_BF16, kv_dtype=_abi.RLDA_BF16, out_dtype=_abi.RLDA_F32, softmax_scale=0.0,
+                kv_stride_page=0, kv_stride_head=0, kv_stride_slot=0, num_work_ranges=0)
+    base.update(kw)
+    for k, v in base.items():
+        setattr(c, k, v)
+    return c
+
+
+def create(lib, c):
+    h = ctypes.c_void_p()
+    st = lib.rl_decode_attn_create(ctypes.byref(c), ctypes.byref(h))
+    return st, h
+
+
+def test_create_accepts_the_workload_configurations(lib):
+    for kw in [dict(num_q_heads=4, num_kv_heads=4, head_dim=64, q_dtype=0, kv_dtype=0, out_dtype=0, max_pages_per_seq=16),
+               dict(),
+               dict(num_q_heads=12, num_kv_heads=2, max_batch=256, max_pages_per_seq=1568),
+               dict(num_q_heads=40, num_kv_heads=8, kv_dtype=_abi.RLDA_FP8_E4M3FN, max_batch=128, max_pages_per_seq=2048),
+               dict(num_q_heads=64, num_kv_heads=8, max_batch=512, max_pages_per_seq=2048, out_dtype=_abi.RLDA_BF16)]:
+        st, h = create(lib, cfg(**kw))
+        assert st == 0, kw
+        n = ctypes.c_size_t()
+        assert lib.rl_decode_attn_workspace_size(h, ctypes.byref(n)) == 0 and n.value > 0 and n.value % 256 == 0
+        assert lib.rl_decode_attn_destroy(h) == 0
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(num_q_heads=30), -1),                     # Hq not a multiple of Hkv
+    (dict(num_kv_heads=0), -1),
+    (dict(max_batch=0), -1),
+    (dict(max_batch=9000), -1),
+    (dict(head_dim=96), -2),
+    (dict(page_size=32), -2),
+    (dict(num_q_heads=68, num_kv_heads=4), -2),     # G = 17 > 16
+    (dict(q_dtype=_abi.RLDA_F32), -2),              # f32 q with bf16 KV
+    (dict(q_dtype=0, kv_dtype=0, out_dtype=0, num_q_heads=8, num_kv_heads=2), -2),   # f32 G*d > 128
+    (dict(kv_stride_page=1000, kv_stride_head=128, kv_stride_slot=100), -1),          # slot stride < d
+    (dict(kv_stride_page=1001 * 8, kv_stride_head=2048, kv_stride_slot=132), -1),      # row not 16-B aligned
+    (dict(softmax_scale=-1.0), -1),
+    (dict(num_work_ranges=5000), -1),
+])
+def test_create_rejects_bad_configurations(lib, kw, want):
+    st, h = create(lib, cfg(**kw))
+    assert st == want and not h.value
+
+
+def test_head_map_must_give_each_kv_head_g_query_heads(lib):
+    c = cfg(num_q_heads=4, num_kv_heads=2)
+    bad = (ctypes.c_int32 * 4)(0, 0, 0, 1)
+    c.kv_head_of_q = bad
+    assert create(lib, c)[0] == -1
+    good = (ctypes.c_int32 * 4)(1, 0, 0, 1)
+    c.kv_head_of_q = good
+    st, h = create(lib, c)
+    assert st == 0
+    lib.rl_decode_attn_destroy(h)
+
+
+def test_run_rejects_bad_arguments_before_launch(lib):
+    st, h = create(lib, cfg())
+    assert st == 0
+    n = ctypes.c_size_t()
+    lib.rl_decode_attn_workspace_size(h, ctypes.byref(n))
+    fake = 0x10000   # never dereferenced: every case fails validation first
+    args = dict(batch=2, num_pages=10, q=fake, k=fake, v=fake, ks=None, vs=None, bt=fake, sl=fake, out=fake,
+                ws=fake * 16, wsb=n.value, stream=None)
+
+    def run(**kw):
+        a = dict(args, **kw)
+        return lib.rl_decode_attn_run(h, a["batch"], a["num_pages"], a["q"], a["k"], a["v"], a["ks"], a["vs"],
+                                      a["bt"], a["sl"], a["out"], a["ws"], a["wsb"], a["stream"])
+
+    assert run(batch=65) == -1            # beyond max_batch
+    assert run(batch=-1) == -1
+    assert run(q=None) == -1
+    assert run(k=fake + 8) == -1          # misaligned cache
+    assert run(out=fake + 4) == -1
+    assert run(bt=fake + 2) == -1
+    assert run(ws=None) == -4
+    assert run(ws=fake * 16 + 64) == -4   # workspace not 256-byte aligned
+    assert run(wsb=n.value - 1) == -4
+    assert run(batch=0) == 0              # nothing to do, nothing launched
+    assert lib.rl_decode_attn_run(None, 1, 1, *([fake] * 8), fake, 1, None) == -1
+    lib.rl_decode_attn_destroy(h)
+
+
+def test_fp8_run_requires_scales(lib):
+    st, h = create(lib, cfg(kv_dtype=_abi.RLDA_FP8_E4M3FN))
+    n = ctypes.c_size_t()
+    lib.rl_decode_attn_workspace_size(h, ctypes.byref(n))
+    f = 0x10000
+    assert lib.rl_decode_attn_run(h, 1, 1, f, f, f, None, None, f, f, f, f * 16, n.value, None) == -1
+    assert lib.rl_decode_attn_run(h, 1, 0, f, None, None, None, None, f, f, f, None, n.value, None) == -4
+    lib.rl_decode_attn_destroy(h)
+
+
+def test_destroy_null_and_strerror(lib):
+    assert lib.rl_decode_attn_destroy(None) == 0
+    for s in (0, -1, -2, -3, -4, -5):
+        assert lib.rl_decode_attn_strerror(s)
+    assert lib.rl_decode_attn_strerror(7) == b"unknown status"
+
+
+def test_workspace_grows_with_forced_ranges_and_heads(lib):
+    sizes = []
+    for kw in [dict(num_work_ranges=16), dict(num_work_ranges=512), dict(num_work_ranges=512, num_q_heads=64, num_kv_heads=4)]:
+        st, h = create(lib, cfg(**kw))
+        n = ctypes.c_size_t()
+        lib.rl_decode_attn_workspace_size(h, ctypes.byref(n))
+        sizes.append(n.value)
+        lib.rl_decode_attn_destroy(h)
+    assert sizes[0] < sizes[1] < sizes[2]
