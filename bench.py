@@ -49,6 +49,27 @@ def cpu_baseline(w, budget_s):
     }
 
 
+def copy_reference(args, torch, dev):
+    """Plain copy of a known byte count (reads N, writes N): the calibration point
+    for FETCH_SIZE / WRITE_SIZE counters."""
+    n = args.copy_mib * 2**20
+    src = torch.ones(n, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(args.warmup):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    print(json.dumps({"mode": "copy", "bytes_read_per_launch": n, "bytes_written_per_launch": n,
+                      "ms_per_launch": round(ms, 5), "GBps_read_plus_write": round(2 * n / (ms * 1e-3) / 1e9, 1)}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -58,6 +79,9 @@ def main():
     ap.add_argument("--sets", type=int, default=3, help="KV pool copies rotated across calls")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of CPU oracle work (0 = skip)")
     ap.add_argument("--ranges", type=int, default=0, help="force the number of work ranges (tuning)")
+    ap.add_argument("--mode", choices=["attention", "copy"], default="attention",
+                    help="copy: a plain device copy of --copy-mib MiB, the reference for HBM counter scaling")
+    ap.add_argument("--copy-mib", type=int, default=256)
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (this path needs no "
@@ -75,6 +99,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+
+    if args.mode == "copy":
+        return copy_reference(args, torch, dev)
 
     log(f"generating {args.workload}")
     w = I.make_workload(args.workload)

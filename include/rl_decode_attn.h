@@ -108,8 +108,9 @@ rlda_status rl_decode_attn_workspace_size(rl_decode_attn_t handle, size_t* bytes
  *   seq_lens     [batch] int32                     0 <= L <= max_pages_per_seq*16
  *   out          [batch][Hq][d]                    out_dtype
  *   workspace    >= rl_decode_attn_workspace_size bytes, 256-byte aligned, zero-filled
- *                before its first use (the contract-flag word accumulates); it holds
- *                partial results between the two kernels of one run.
+ *                before its first use.  It holds per-segment counters that every run
+ *                returns to zero, partial results, and the contract-flag word (which
+ *                accumulates).  Calls that may overlap in time need separate workspaces.
  * Pointers q, k_cache, v_cache and out must be 16-byte aligned; with num_pages == 0
  * (all sequences empty) the cache and scale pointers may be NULL.
  * Device-side contract violations (a page id outside the pool, a length beyond
@@ -124,8 +125,7 @@ rlda_status rl_decode_attn_run(rl_decode_attn_t handle, int32_t batch, int32_t n
 
 /* As rl_decode_attn_run, and records the caller's hipEvent_t `event_begin` /
  * `event_end` on `stream` immediately before and after the attention kernel (the
- * kernel that streams the KV cache; a small merge kernel follows it), so callers can
- * time that kernel alone.  Both events are required. */
+ * run's only kernel), so callers can time it alone.  Both events are required. */
 rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t handle, int32_t batch, int32_t num_pages, const void* q,
                                         const void* k_cache, const void* v_cache, const float* k_scale,
                                         const float* v_scale, const int32_t* block_table,

@@ -20,28 +20,27 @@ struct rlda_handle {
   float scale;
   int16_t q_head[rlda::kMaxQHeads];
   rlda::KvKind kind;
-  int32_t occupancy;                               // workgroups per CU, queried on first run
 };
 
 namespace {
 
 constexpr size_t kAlign = 256;
-constexpr int kDefaultWsRanges = 2048;   // covers up to 8 workgroups per CU on 256 CUs
+constexpr int kDefaultWsRanges = 1024;   // default work ranges = CU count (256 on MI355X)
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 int elem_bytes(rlda_dtype t) { return t == RLDA_F32 ? 4 : t == RLDA_BF16 ? 2 : 1; }
 
 struct WsLayout {
-  size_t flags, seg_pre, part_ml, part_acc, total;
+  size_t flags, counters, part_ml, part_acc, total;
 };
 
 WsLayout layout_of(const rlda_handle* h) {
   const rl_decode_attn_config& c = h->cfg;
   WsLayout w;
   w.flags = 0;
-  w.seg_pre = align_up(sizeof(uint32_t));
-  w.part_ml = align_up(w.seg_pre + sizeof(int32_t) * ((size_t)c.max_batch + 1));
+  w.counters = align_up(sizeof(uint32_t));
+  w.part_ml = align_up(w.counters + sizeof(uint32_t) * (size_t)c.max_batch * c.num_kv_heads);
   w.part_acc = align_up(w.part_ml + sizeof(float) * 2 * (size_t)h->ws_ranges * h->group * 2);
   w.total = align_up(w.part_acc + sizeof(float) * 2 * (size_t)h->ws_ranges * h->group * c.head_dim);
   return w;
@@ -133,7 +132,6 @@ rlda_status rl_decode_attn_create(const rl_decode_attn_config* cfg, rl_decode_at
   hd->scale = c.softmax_scale > 0.f ? c.softmax_scale : (float)(1.0 / sqrt((double)c.head_dim));
   memcpy(hd->q_head, q_head, sizeof q_head);
   hd->kind = kind;
-  hd->occupancy = 0;
   *out_handle = hd;
   return RLDA_OK;
 }
@@ -170,16 +168,12 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, const
 
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return RLDA_ERR_HIP;
+  // One workgroup (one wave per SIMD) per CU by default: a second workgroup on a
+  // CU would lose instruction arbitration to the first and finish its share later.
   int ranges = c.num_work_ranges;
   if (ranges == 0) {
-    const int cus = cu_count(dev);
-    int occ = __atomic_load_n(&h->occupancy, __ATOMIC_RELAXED);
-    if (occ == 0) {
-      occ = rlda::occupancy_per_cu(h->kind, c.head_dim, h->group);
-      __atomic_store_n(&h->occupancy, occ, __ATOMIC_RELAXED);
-    }
-    if (cus <= 0 || occ <= 0) return RLDA_ERR_HIP;
-    ranges = cus * occ;
+    ranges = cu_count(dev);
+    if (ranges <= 0) return RLDA_ERR_HIP;
   }
   if (ranges > h->ws_ranges) ranges = h->ws_ranges;
   if (ranges > rlda::kMaxRanges) ranges = rlda::kMaxRanges;
@@ -199,7 +193,7 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, const
   p.seq_lens = seq_lens;
   p.out = out;
   p.flags = (uint32_t*)(ws + wl.flags);
-  p.seg_pre = (int32_t*)(ws + wl.seg_pre);
+  p.counters = (uint32_t*)(ws + wl.counters);
   p.part_ml = (float*)(ws + wl.part_ml);
   p.part_acc = (float*)(ws + wl.part_acc);
   const int eb = elem_bytes(c.kv_dtype);

@@ -22,13 +22,15 @@
 //      registers are already the P^T operand, and V's operand is assembled from
 //      4 row loads per lane, so neither operand goes through LDS.
 //   5. Merge.  The 4 waves' (max, sum, O) are merged through LDS.  A piece that
-//      is a whole (sequence, KV head) is normalised and written; otherwise its
-//      unnormalised partial goes to the workspace.
-//   6. A second, small kernel merges the partials of every split (sequence, KV
-//      head) in a fixed order with log-sum-exp weights and writes zero rows for
-//      empty sequences.  The launch boundary is what makes the partials visible
-//      across XCDs; no workgroup waits on another and no device-scope fence is
-//      issued per piece (each such fence writes back and invalidates an XCD's L2).
+//      is a whole (sequence, KV head) is normalised and written.  A piece of a
+//      segment that is split across workgroups stores its unnormalised partial
+//      with device-scope (sc1) stores, which write through the XCD's L2; after
+//      they complete, the workgroup bumps the segment's counter.  The workgroup
+//      that completes the count reads every piece of the segment with
+//      device-scope loads, merges them in piece order with log-sum-exp weights,
+//      writes the output and resets the counter.  No workgroup waits for another,
+//      and no device-scope fence (a whole-L2 writeback and invalidate per XCD) is
+//      issued.
 // fp8 (OCP E4M3FN) caches are converted exactly to bf16 for the MFMA; the K
 // scale multiplies the scores and the V scale multiplies P.  fp32 caches use a
 // VALU path.
@@ -51,8 +53,8 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 #define RLDA_MFMA_DEPTH 3                    // pages in flight per wave, MFMA path
 #endif
 constexpr int kChunk = 64;                   // page ids fetched per vector load
-constexpr int kMergeGrid = 1024;             // workgroups of the merge kernel (grid-stride)
 constexpr uint32_t kRsrcWord3 = 0x00020000u; // raw buffer, 32-bit data format
+constexpr int kLoadNT = 2;                   // cache policy: non-temporal (KV is read once)
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_huge_valf(); }
 
@@ -75,21 +77,21 @@ template <>
 struct RowLoad<16> {
   typedef u32x4 type;
   static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
-    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kLoadNT);
   }
 };
 template <>
 struct RowLoad<8> {
   typedef u32x2 type;
   static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
-    return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+    return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kLoadNT);
   }
 };
 template <>
 struct RowLoad<4> {
   typedef uint32_t type;
   static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
-    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kLoadNT);
   }
 };
 
@@ -118,6 +120,71 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
+
+// ---------------------------------------------------------------- helpers
+
+__device__ __forceinline__ int64_t owner_of(int64_t x, int W, int64_t T) {
+  // Largest u with floor(u*T/W) <= x.
+  return ((x + 1) * (int64_t)W - 1) / T;
+}
+
+// Write N consecutive output elements o[0..N) * inv of row (b, qh) starting at d0.
+template <int D, int N>
+__device__ __forceinline__ void store_row(const Params& p, int b, int qh, int d0, const float* o, float inv) {
+  const int64_t base = ((int64_t)b * p.num_q_heads + qh) * D + d0;
+  if (p.out_bf16) {
+    uint32_t* dst = (uint32_t*)((uint16_t*)p.out + base);
+#pragma unroll
+    for (int k = 0; k < N / 2; ++k) dst[k] = pack_bf16(o[2 * k] * inv, o[2 * k + 1] * inv);
+  } else {
+    float* dst = (float*)p.out + base;
+#pragma unroll
+    for (int k = 0; k < N; k += 4) *(f32x4*)(dst + k) = f32x4{o[k] * inv, o[k + 1] * inv, o[k + 2] * inv, o[k + 3] * inv};
+  }
+}
+template <int D>
+__device__ __forceinline__ void store_out(const Params& p, int b, int qh, int d0, const float* o, float inv) {
+  store_row<D, D / 16>(p, b, qh, d0, o, inv);
+}
+
+// Device-scope (sc1) store / load: coherent across XCDs without L2 maintenance.
+__device__ __forceinline__ void store_device(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_device(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Merge the pieces of segment (b, g) held by workgroups u_first..u_last: the piece
+// of workgroup k is in slot 2k+1 when it continues past k's share, else in slot 2k.
+// One pass in piece order with a running maximum.  Thread (h, d0) writes its
+// D/16 outputs.
+template <int D>
+__device__ __forceinline__ void merge_pieces(const Params& p, int b, int g, int h, int d0, int64_t u_first,
+                                             int64_t u_last) {
+  constexpr int DPT = D / 16;
+  const int G = p.group;
+  float M = neg_inf(), Ls = 0.f, o[DPT];
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) o[e] = 0.f;
+#pragma unroll 2
+  for (int64_t k = u_first; k <= u_last; ++k) {
+    const int64_t sl = (k < u_last) ? 2 * k + 1 : 2 * k;
+    const float mk = load_device(p.part_ml + (sl * G + h) * 2);
+    const float lk = load_device(p.part_ml + (sl * G + h) * 2 + 1);
+    float v[DPT];
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) v[e] = load_device(p.part_acc + (sl * G + h) * D + d0 + e);
+    if (mk == neg_inf()) continue;
+    const float Mn = fmaxf(M, mk);
+    const float a_old = __builtin_amdgcn_exp2f(M - Mn), a_new = __builtin_amdgcn_exp2f(mk - Mn);
+    Ls = Ls * a_old + lk * a_new;
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) o[e] = o[e] * a_old + v[e] * a_new;
+    M = Mn;
+  }
+  store_out<D>(p, b, p.q_head[g * G + h], d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
+}
 
 // ---------------------------------------------------------------- MFMA policy
 // Lane l = 16q + i (q = lane group 0..3, i = 0..15).
@@ -177,7 +244,7 @@ struct Mfma {
 
   __device__ __forceinline__ void issue(Frag& f, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv) const {
 #pragma unroll
-    for (int s = 0; s < KL; ++s) f.k[s] = __builtin_amdgcn_raw_buffer_load_b128(rk, koff[s], 0, 0);
+    for (int s = 0; s < KL; ++s) f.k[s] = RowLoad<16>::load(rk, koff[s]);
 #pragma unroll
     for (int r = 0; r < 4; ++r) f.v[r] = RowLoad<VB>::load(rv, voff[r]);
   }
@@ -274,6 +341,19 @@ struct Mfma {
       sml[i][1] = lt;
     }
   }
+
+  // A piece this wave covered entirely: normalise and write its rows.
+  __device__ __forceinline__ void write_out(const Params& p, int b, int g, int lane) const {
+    const int i = lane & 15, qg = lane >> 4;
+    const float lt = group_sum(l);
+    if (i >= p.group) return;
+    float o[4 * DT];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int t = 0; t < DT; ++t) o[r * DT + t] = acc[t][r];
+    store_row<D, 4 * DT>(p, b, p.q_head[g * p.group + i], 4 * DT * qg, o, lt > 0.f ? 1.f / lt : 0.f);
+  }
 };
 
 // ---------------------------------------------------------------- VALU policy (fp32 KV)
@@ -315,9 +395,9 @@ struct Valu {
 
   __device__ __forceinline__ void issue(Frag& f, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv) const {
 #pragma unroll
-    for (int s = 0; s < NL; ++s) f.k[s] = __builtin_amdgcn_raw_buffer_load_b128(rk, off + 16 * s, 0, 0);
+    for (int s = 0; s < NL; ++s) f.k[s] = RowLoad<16>::load(rk, off + 16 * s);
 #pragma unroll
-    for (int s = 0; s < NL; ++s) f.v[s] = __builtin_amdgcn_raw_buffer_load_b128(rv, off + 16 * s, 0, 0);
+    for (int s = 0; s < NL; ++s) f.v[s] = RowLoad<16>::load(rv, off + 16 * s);
   }
 
   __device__ __forceinline__ void compute(const Frag& f, int lane, int valid_tokens, float kmul, float) {
@@ -345,71 +425,67 @@ struct Valu {
     }
   }
 
-  __device__ __forceinline__ void to_lds(float (*sacc)[D + 4], float (*sml)[2], int lane) {
-    const int c = lane & 3;
+  // Sum the per-token-slot partial sums over the 16 token slots (lanes 4t + c).
+  __device__ __forceinline__ void reduce_tokens(float* lt) {
 #pragma unroll
     for (int h = 0; h < GM; ++h) {
-      float lt = l[h];
+      float a = l[h];
 #pragma unroll
-      for (int o = 4; o < 64; o <<= 1) lt += __shfl_xor(lt, o);
+      for (int o = 4; o < 64; o <<= 1) a += __shfl_xor(a, o);
+      lt[h] = a;
 #pragma unroll
       for (int j = 0; j < CW; ++j) {
-        float a = acc[h][j];
+        float v = acc[h][j];
 #pragma unroll
-        for (int o = 4; o < 64; o <<= 1) a += __shfl_xor(a, o);
-        acc[h][j] = a;
+        for (int o = 4; o < 64; o <<= 1) v += __shfl_xor(v, o);
+        acc[h][j] = v;
       }
+    }
+  }
+
+  __device__ __forceinline__ void to_lds(float (*sacc)[D + 4], float (*sml)[2], int lane) {
+    const int c = lane & 3;
+    float lt[GM];
+    reduce_tokens(lt);
+#pragma unroll
+    for (int h = 0; h < GM; ++h) {
       if (lane < 4) {
 #pragma unroll
         for (int j = 0; j < CW; ++j) sacc[h][c * CW + j] = acc[h][j];
       }
       if (lane == 0) {
         sml[h][0] = m[h];
-        sml[h][1] = lt;
+        sml[h][1] = lt[h];
       }
     }
   }
-};
 
-// ---------------------------------------------------------------- helpers
-
-__device__ __forceinline__ int64_t owner_of(int64_t x, int W, int64_t T) {
-  // Largest u with floor(u*T/W) <= x.
-  return ((x + 1) * (int64_t)W - 1) / T;
-}
-
-template <int D>
-__device__ __forceinline__ void store_out(const Params& p, int b, int qh, int d0, const float* o, float inv) {
-  constexpr int N = D / 16;
-  const int64_t base = ((int64_t)b * p.num_q_heads + qh) * D + d0;
-  if (p.out_bf16) {
-    uint32_t w[N / 2];
+  __device__ __forceinline__ void write_out(const Params& p, int b, int g, int lane) {
+    const int c = lane & 3;
+    float lt[GM];
+    reduce_tokens(lt);
+    if (lane >= 4) return;
 #pragma unroll
-    for (int k = 0; k < N / 2; ++k) w[k] = pack_bf16(o[2 * k] * inv, o[2 * k + 1] * inv);
-    uint32_t* dst = (uint32_t*)((uint16_t*)p.out + base);
-#pragma unroll
-    for (int k = 0; k < N / 2; ++k) dst[k] = w[k];
-  } else {
-    float* dst = (float*)p.out + base;
-#pragma unroll
-    for (int k = 0; k < N; k += 4) {
-      f32x4 v = {o[k] * inv, o[k + 1] * inv, o[k + 2] * inv, o[k + 3] * inv};
-      *(f32x4*)(dst + k) = v;
-    }
+    for (int h = 0; h < GM; ++h)
+      if (h < p.group) store_row<D, CW>(p, b, p.q_head[g * p.group + h], c * CW, acc[h], lt[h] > 0.f ? 1.f / lt[h] : 0.f);
   }
-}
+};
 
 // ---------------------------------------------------------------- the kernel
 
 template <class Pol>
-__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(2, 2)))
+__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(1, 1)))
 void decode_attention_kernel(const Params p) {
   constexpr int D = Pol::kD;
-  constexpr int DPT = D / 16;   // output elements per thread in the merge
+  constexpr int DPT = D / 16;   // output elements per thread in the workgroup merge
   __shared__ int32_t s_pre[kMaxBatch + 1];
-  __shared__ float s_acc[kWaves][16][D + 4];
-  __shared__ float s_ml[kWaves][16][2];
+  // Cut pieces: slot 2w holds wave w's piece that began before its quarter of the
+  // share, slot 2w+1 its piece that continues past it.
+  __shared__ float s_acc[2 * kWaves][16][D + 4];
+  __shared__ float s_ml[2 * kWaves][16][2];
+  __shared__ int32_t s_seg[2 * kWaves];
   __shared__ int32_t s_scan[kWaves];
+  __shared__ int32_t s_last[2];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
   const int u = blockIdx.x, W = p.nranges;
@@ -437,6 +513,7 @@ void decode_attention_kernel(const Params p) {
       if (lane >= o) x += y;
     }
     if (lane == 63) s_scan[wave] = x;
+    if (tid < 2 * kWaves) s_seg[tid] = -1;
     __syncthreads();
     int run = x - sum;
     for (int w = 0; w < wave; ++w) run += s_scan[w];
@@ -449,24 +526,37 @@ void decode_attention_kernel(const Params p) {
   }
   const int64_t T = uni64((int64_t)s_pre[batch] * Hkv);
 
-  // 2. The merge kernel reuses the prefix sums.
-  if (u == 0) {
-    for (int b = tid; b <= batch; b += kThreads) p.seg_pre[b] = s_pre[b];
+  // 2. Sequences with no tokens get zero rows.
+  for (int b = u; b < batch; b += W) {
+    if (s_pre[b + 1] != s_pre[b]) continue;
+    const int n = p.num_q_heads * D;
+    for (int e = tid; e < n; e += kThreads) {
+      if (p.out_bf16)
+        ((uint16_t*)p.out)[(int64_t)b * n + e] = 0;
+      else
+        ((float*)p.out)[(int64_t)b * n + e] = 0.f;
+    }
   }
 
   // Never more shares than units: every share below Wn is non-empty.
   const int Wn = (int)min((int64_t)W, T);
   if (u >= Wn) return;
 
-  // 3. This workgroup's share [r0, r1) of the flattened (sequence, KV head, page) list.
+  // 3. This workgroup's share [r0, r1) of the flattened (sequence, KV head, page)
+  //    list, and this wave's quarter [w0, w1) of it.  Each wave walks its own
+  //    pieces without waiting for the others; a piece inside its quarter is
+  //    written directly.
   const int64_t r0 = (int64_t)u * T / Wn, r1 = (int64_t)(u + 1) * T / Wn;
-  int64_t x = r0;
-  while (x < r1) {
-    const int64_t y = x / Hkv;
+  const int64_t w0 = r0 + (r1 - r0) * wave / kWaves, w1 = r0 + (r1 - r0) * (wave + 1) / kWaves;
+  int64_t x = w0;
+  while (x < w1) {
     int lo = 0, hi = batch;   // s_pre[lo] <= y < s_pre[hi]
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (s_pre[mid] <= y) lo = mid; else hi = mid;
+    {
+      const int64_t y = x / Hkv;
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (s_pre[mid] <= y) lo = mid; else hi = mid;
+      }
     }
     const int b = uni(lo);
     const int pre_b = uni(s_pre[b]);
@@ -474,23 +564,17 @@ void decode_attention_kernel(const Params p) {
     const int64_t off = x - (int64_t)Hkv * pre_b;
     const int g = (int)(off / nb);
     const int j0 = (int)(off % nb);
-    const int64_t seg_start = x - j0, seg_end = seg_start + nb;
-    const int64_t pe = min(r1, seg_end);
+    const int64_t seg_end = x - j0 + nb;
+    const int64_t pe = min(w1, seg_end);
     const int j1 = j0 + (int)(pe - x);
-    const bool whole = (j0 == 0) && (pe == seg_end);
     const int len = min(max(p.seq_lens[b], 0), cap);
-
-    // 3a. This wave's contiguous run of the piece's pages.
-    const int np = j1 - j0;
-    const int per = (np + kWaves - 1) / kWaves;
-    const int ja = min(j0 + wave * per, j1), jb = min(ja + per, j1);
 
     Pol st;
     st.init(p, b, g, lane, p.stride_slot);
     const char* kg = (const char*)p.k + (int64_t)g * p.stride_head;
     const char* vg = (const char*)p.v + (int64_t)g * p.stride_head;
-    for (int cb = ja; cb < jb; cb += kChunk) {
-      const int cn = min(kChunk, jb - cb);
+    for (int cb = j0; cb < j1; cb += kChunk) {
+      const int cn = min(kChunk, j1 - cb);
       int pid = p.block_table[(int64_t)b * p.max_pages + cb + min(lane, cn - 1)];
       if ((unsigned)pid >= (unsigned)p.num_pages) {
         atomicOr(p.flags, kFlagBadPage);
@@ -534,96 +618,92 @@ void decode_attention_kernel(const Params p) {
         }
       }
     }
-    st.to_lds(s_acc[wave], s_ml[wave], lane);
-    __syncthreads();
+    const bool before = j0 > 0;            // the segment began before this quarter
+    const bool after = pe < seg_end;       // ... or continues past it
+    if (!before && !after) {
+      st.write_out(p, b, g, lane);
+    } else {
+      const int slot = 2 * wave + (after ? 1 : 0);
+      st.to_lds(s_acc[slot], s_ml[slot], lane);
+      if (lane == 0) s_seg[slot] = b * Hkv + g;
+    }
+    x = pe;
+  }
+  __syncthreads();
 
-    // 3b. Merge the four waves; write the output or this piece's partial.
-    const int h = tid >> 4, d0 = (tid & 15) * DPT;
-    const bool after = (pe == r1) && (pe < seg_end);
-    const int slot = after ? 2 * u + 1 : 2 * u;
+  // 4. Merge the cut pieces in position order.  The used slots holding one segment
+  //    are consecutive; together they are either the whole segment (normalise and
+  //    write) or this workgroup's piece of a segment cut at the share boundary
+  //    (published as a partial).
+  const int h = tid >> 4, d0 = (tid & 15) * DPT;
+  int hand_seg[2] = {-1, -1};
+  int nhand = 0;
+  for (int k = 0; k < 2 * kWaves;) {
+    const int sgi = s_seg[k];
+    if (sgi < 0) {
+      ++k;
+      continue;
+    }
+    int k1 = k + 1;
+    while (k1 < 2 * kWaves && (s_seg[k1] == sgi || s_seg[k1] < 0)) ++k1;
+    const int b = sgi / Hkv, g = sgi - b * Hkv;
+    const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
+    const int64_t seg_start = (int64_t)Hkv * pre_b + (int64_t)g * nb, seg_end = seg_start + nb;
+    const bool whole = seg_start >= r0 && seg_end <= r1;
     if (h < G) {
-      float mw[kWaves], M = neg_inf();
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
-        mw[w] = s_ml[w][h][0];
-        M = fmaxf(M, mw[w]);
-      }
+      float M = neg_inf();
+      for (int j = k; j < k1; ++j)
+        if (s_seg[j] == sgi) M = fmaxf(M, s_ml[j][h][0]);
       float Ls = 0.f, o[DPT];
 #pragma unroll
       for (int e = 0; e < DPT; ++e) o[e] = 0.f;
+      for (int j = k; j < k1; ++j) {
+        if (s_seg[j] != sgi) continue;
+        const float mj = s_ml[j][h][0];
+        const float a = (mj == neg_inf()) ? 0.f : __builtin_amdgcn_exp2f(mj - M);
+        Ls += a * s_ml[j][h][1];
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
-        const float a = (mw[w] == neg_inf()) ? 0.f : __builtin_amdgcn_exp2f(mw[w] - M);
-        Ls += a * s_ml[w][h][1];
-#pragma unroll
-        for (int e = 0; e < DPT; ++e) o[e] += a * s_acc[w][h][d0 + e];
+        for (int e = 0; e < DPT; ++e) o[e] += a * s_acc[j][h][d0 + e];
       }
       if (whole) {
         store_out<D>(p, b, p.q_head[g * G + h], d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
       } else {
-        float* dst = p.part_acc + ((int64_t)slot * G + h) * D + d0;
+        const int64_t gs = (seg_end > r1) ? 2 * (int64_t)u + 1 : 2 * (int64_t)u;
+        float* dst = p.part_acc + (gs * G + h) * D + d0;
 #pragma unroll
-        for (int e = 0; e < DPT; e += 4) *(f32x4*)(dst + e) = f32x4{o[e], o[e + 1], o[e + 2], o[e + 3]};
+        for (int e = 0; e < DPT; ++e) store_device(dst + e, o[e]);
         if ((tid & 15) == 0) {
-          p.part_ml[((int64_t)slot * G + h) * 2] = M;
-          p.part_ml[((int64_t)slot * G + h) * 2 + 1] = Ls;
+          store_device(p.part_ml + (gs * G + h) * 2, M);
+          store_device(p.part_ml + (gs * G + h) * 2 + 1, Ls);
         }
       }
     }
-
-    __syncthreads();
-    x = pe;
+    if (!whole && nhand < 2) hand_seg[nhand++] = sgi;   // only the first and last group can be cut
+    k = k1;
   }
-}
 
-// Split (sequence, KV head) segments: merge their pieces in piece order with
-// log-sum-exp weights.  Empty sequences: zero rows.  One thread per
-// (query head of the group, D/16 output elements); no inter-thread traffic.
-template <int D>
-__global__ __launch_bounds__(kThreads) void merge_pieces_kernel(const Params p) {
-  constexpr int DPT = D / 16;
-  const int tid = threadIdx.x;
-  const int h = tid >> 4, d0 = (tid & 15) * DPT;
-  const int batch = p.batch, Hkv = p.num_kv_heads, G = p.group;
-  if (h >= G) return;
-  const int64_t T = (int64_t)p.seg_pre[batch] * Hkv;
-  const int Wn = (int)min((int64_t)p.nranges, T);
-  const int nseg = batch * Hkv;
-  for (int sgi = blockIdx.x; sgi < nseg; sgi += gridDim.x) {
+  // 5. Segments cut at the share boundary: count this piece; the workgroup that
+  //    completes the count merges every piece of the segment and resets the count.
+  if (nhand == 0) return;
+  __builtin_amdgcn_s_waitcnt(0);   // this wave's device-scope stores have completed
+  __syncthreads();                 // ... and every other wave's
+  if (tid < nhand) {
+    const int sgi = hand_seg[tid];
     const int b = sgi / Hkv, g = sgi - b * Hkv;
-    const int pre_b = p.seg_pre[b], nb = p.seg_pre[b + 1] - pre_b;
-    const int qh = p.q_head[g * G + h];
-    float o[DPT];
-#pragma unroll
-    for (int e = 0; e < DPT; ++e) o[e] = 0.f;
-    if (nb == 0) {
-      store_out<D>(p, b, qh, d0, o, 0.f);
-      continue;
-    }
-    const int64_t seg_start = (int64_t)Hkv * pre_b + (int64_t)g * nb, seg_end = seg_start + nb;
-    const int64_t u_first = owner_of(seg_start, Wn, T), u_last = owner_of(seg_end - 1, Wn, T);
-    if (u_first == u_last) continue;   // written whole by the attention kernel
-    // piece of workgroup k: slot 2k+1 when it continues past k's share, else slot 2k
-    float M = neg_inf();
-    for (int64_t k = u_first; k <= u_last; ++k) {
-      const int64_t sl = (k < u_last) ? 2 * k + 1 : 2 * k;
-      M = fmaxf(M, p.part_ml[(sl * G + h) * 2]);
-    }
-    float Ls = 0.f;
-    for (int64_t k = u_first; k <= u_last; ++k) {
-      const int64_t sl = (k < u_last) ? 2 * k + 1 : 2 * k;
-      const float mk = p.part_ml[(sl * G + h) * 2];
-      const float a = (mk == neg_inf()) ? 0.f : __builtin_amdgcn_exp2f(mk - M);
-      Ls += a * p.part_ml[(sl * G + h) * 2 + 1];
-      const f32x4* src = (const f32x4*)(p.part_acc + (sl * G + h) * D + d0);
-#pragma unroll
-      for (int e = 0; e < DPT / 4; ++e) {
-        const f32x4 v = src[e];
-#pragma unroll
-        for (int c = 0; c < 4; ++c) o[4 * e + c] += a * v[c];
-      }
-    }
-    store_out<D>(p, b, qh, d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
+    const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
+    const int64_t seg_start = (int64_t)Hkv * pre_b + (int64_t)g * nb;
+    const uint32_t npieces = (uint32_t)(owner_of(seg_start + nb - 1, Wn, T) - owner_of(seg_start, Wn, T) + 1);
+    s_last[tid] = (atomicAdd(p.counters + sgi, 1u) + 1u == npieces);
+  }
+  __syncthreads();
+  for (int i = 0; i < nhand; ++i) {
+    if (!s_last[i]) continue;
+    const int sgi = hand_seg[i];
+    const int b = sgi / Hkv, g = sgi - b * Hkv;
+    const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
+    const int64_t seg_start = (int64_t)Hkv * pre_b + (int64_t)g * nb;
+    if (h < G) merge_pieces<D>(p, b, g, h, d0, owner_of(seg_start, Wn, T), owner_of(seg_start + nb - 1, Wn, T));
+    if (tid == 0) atomicExch(p.counters + sgi, 0u);
   }
 }
 
@@ -635,18 +715,7 @@ int launch(const Params& p, void* stream, void* ev_begin, void* ev_end) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
   if (ev_end && hipEventRecord((hipEvent_t)ev_end, st) != hipSuccess) return -1;
-  const int nseg = p.batch * p.num_kv_heads;
-  const int grid = nseg < kMergeGrid ? nseg : kMergeGrid;
-  hipLaunchKernelGGL(merge_pieces_kernel<Pol::kD>, dim3(grid), dim3(kThreads), 0, st, p);
-  return (int)hipGetLastError();
-}
-
-template <class Pol>
-int occupancy() {
-  int n = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_attention_kernel<Pol>, kThreads, 0) != hipSuccess)
-    return 0;
-  return n;
+  return 0;
 }
 
 }  // namespace
@@ -670,6 +739,5 @@ int launch_decode(KvKind kind, int head_dim, int group, const Params& p, void* s
   RLDA_DISPATCH(launch, p, stream, ev_begin, ev_end)
 }
 
-int occupancy_per_cu(KvKind kind, int head_dim, int group) { RLDA_DISPATCH(occupancy, ) }
 
 }  // namespace rlda

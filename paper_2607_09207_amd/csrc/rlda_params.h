@@ -5,7 +5,7 @@
 namespace rlda {
 
 constexpr int kPage = 16;          // tokens per KV page
-constexpr int kWaves = 4;          // waves per workgroup
+constexpr int kWaves = 4;          // waves per workgroup: one per SIMD, one workgroup per CU
 constexpr int kThreads = 64 * kWaves;
 constexpr int kMaxQHeads = 256;
 constexpr int kMaxBatch = 8192;
@@ -27,7 +27,7 @@ struct Params {
   void* out;                   // [batch][Hq][D]
   float* part_acc;             // [2 * nranges][G][D]  unnormalised partial outputs
   float* part_ml;              // [2 * nranges][G][2]  (running max in log2 units, sum)
-  int32_t* seg_pre;            // [batch + 1] page-count prefix sums, for the merge kernel
+  uint32_t* counters;          // [max_batch * Hkv] finished pieces per split segment; zero between runs
   uint32_t* flags;             // contract-violation bits
   int64_t stride_page;         // bytes
   int64_t stride_head;         // bytes
@@ -47,9 +47,8 @@ struct Params {
 enum class KvKind { F32, BF16, FP8 };
 
 // Kernel launchers (rlda_kernels.hip).  Return hipSuccess or the launch error.
-// The attention kernel is bracketed by ev_begin / ev_end when they are non-null.
+// The kernel is bracketed by ev_begin / ev_end when they are non-null.
 int launch_decode(KvKind kind, int head_dim, int group, const Params& p, void* stream, void* ev_begin,
                   void* ev_end);
-int occupancy_per_cu(KvKind kind, int head_dim, int group);
 
 }  // namespace rlda

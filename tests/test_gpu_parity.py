@@ -242,3 +242,32 @@ def test_functional_api_and_profiled_events(torch_cuda):
     torch.cuda.synchronize()
     assert e0.elapsed_time(e1) > 0.0
     assert torch.equal(out, out2)
+
+
+def test_split_merge_handoff_under_repetition(torch_cuda):
+    """Pieces of split segments are handed between workgroups (possibly on different
+    XCDs) through the workspace.  Two inputs alternate through one workspace; a
+    partial read before it was published, or left over from the other input, would
+    change the output."""
+    torch = torch_cuda
+    wa = I.make_custom([3000, 20, 1700, 9, 800, 5000, 1], 28, 4, 128, q_dtype="bf16", kv_dtype="bf16", seed=31)
+    wb = I.make_custom([2500, 700, 33, 4100, 1, 16, 900], 28, 4, 128, q_dtype="bf16", kv_dtype="bf16", seed=33,
+                       max_pages_per_seq=wa.max_pages_per_seq)
+    h = handle_for(wa, ranges=300)
+    ta, tb = I.to_torch(wa, "cuda"), I.to_torch(wb, "cuda")
+    args = lambda t: (t["q"], t["k_cache"], t["v_cache"], t["block_table"], t["seq_lens"])
+    log("handoff stress: 2 x 40 alternating calls, 300 work ranges")
+    ref_a = h(*args(ta)).clone()
+    ref_b = h(*args(tb)).clone()
+    torch.cuda.synchronize()
+    assert_close(ref_a.double().cpu().numpy(), oracle.run(wa), "bf16", "handoff a")
+    assert_close(ref_b.double().cpu().numpy(), oracle.run(wb), "bf16", "handoff b")
+    bad = 0
+    out = torch.empty_like(ref_a)
+    for it in range(40):
+        h(*args(ta), out=out)
+        bad += int(not torch.equal(out, ref_a))
+        h(*args(tb), out=out)
+        bad += int(not torch.equal(out, ref_b))
+    torch.cuda.synchronize()
+    assert bad == 0
