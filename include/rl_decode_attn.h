@@ -75,7 +75,9 @@ typedef struct {
   int32_t head_dim;               /* d: 64 or 128 */
   int32_t page_size;              /* P: 16 */
   int32_t max_batch;              /* largest batch passed to run, 1..8192 */
-  int32_t max_pages_per_seq;      /* block_table row length (elements) */
+  int32_t max_pages_per_seq;      /* block_table row length (elements); max_batch *
+                                     max_pages_per_seq * num_kv_heads <= 2^31 - 1,
+                                     else RLDA_ERR_UNSUPPORTED                       */
   rlda_dtype q_dtype, kv_dtype, out_dtype;
   const int32_t* kv_head_of_q;    /* HOST array [Hq] copied at create; NULL = h / G.
                                      Every KV head must receive exactly G query heads. */

@@ -84,6 +84,8 @@ rlda_status rl_decode_attn_create(const rl_decode_attn_config* cfg, rl_decode_at
     return RLDA_ERR_INVALID_ARG;
   if (c.page_size != rlda::kPage) return RLDA_ERR_UNSUPPORTED;
   if (c.head_dim != 64 && c.head_dim != 128) return RLDA_ERR_UNSUPPORTED;
+  // The kernel numbers (sequence, KV head, page) units with 32-bit integers.
+  if ((int64_t)c.max_batch * c.max_pages_per_seq * c.num_kv_heads > INT32_MAX) return RLDA_ERR_UNSUPPORTED;
   const int G = c.num_q_heads / c.num_kv_heads;
 
   rlda::KvKind kind;

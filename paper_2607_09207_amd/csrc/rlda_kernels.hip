@@ -10,23 +10,28 @@
 //      are therefore cut across many workgroups and short ones packed together:
 //      every workgroup streams the same number of KV pages however long the tail
 //      of the length distribution is (Sec. 2.3 on long-tail decode).
-//   2. Page gather.  Within a share, each maximal run of pages of one
-//      (sequence, KV head) is a "piece"; its pages are split among the 4 waves.
-//      A wave keeps 2-3 pages in flight in registers using buffer loads whose
-//      range check returns zero past a page's last valid token, so masked slots
-//      and pages past the piece cost no memory traffic and never yield NaN.
+//   2. Page gather.  Each of the 4 waves of a workgroup takes a quarter of the
+//      share and walks it as one continuous stream of pages: its lanes decode 64
+//      positions at a time (sequence, KV head, page id, valid tokens, segment
+//      start/end flags) one chunk ahead of use, and the wave keeps 3 pages in
+//      flight in registers with buffer loads whose range check returns zero past
+//      a page's last valid token, so masked slots cost no memory traffic and
+//      never yield NaN.  A segment's Q operand is loaded with its first page.
+//      Segment boundaries inside the stream cost no pipeline restart.
 //   3. Scores and softmax.  All G query heads that share the KV head are packed
 //      into one 16-row MFMA tile: S^T = K Q^T with v_mfma_f32_16x16x32_bf16; the
-//      online softmax keeps a running max and sum per head in log2 units.
+//      online softmax keeps a running reference max and sum per head in log2
+//      units, and moves the reference (rescaling the accumulator) only when a
+//      score exceeds it by more than 8, i.e. a probability above 2^8.
 //   4. PV.  O^T += V^T P^T with v_mfma_f32_16x16x16_bf16: the score tile's output
 //      registers are already the P^T operand, and V's operand is assembled from
 //      4 row loads per lane, so neither operand goes through LDS.
-//   5. Merge.  The 4 waves' (max, sum, O) are merged through LDS.  A piece that
-//      is a whole (sequence, KV head) is normalised and written.  A piece of a
-//      segment that is split across workgroups stores its unnormalised partial
-//      with device-scope (sc1) stores, which write through the XCD's L2; after
-//      they complete, the workgroup bumps the segment's counter.  The workgroup
-//      that completes the count reads every piece of the segment with
+//   5. Merge.  A segment a wave covered whole is normalised and written by that
+//      wave.  The cut pieces (at most 2 per wave) are merged through LDS.  A piece
+//      of a segment that is split across workgroups stores its unnormalised
+//      partial with device-scope (sc1) stores, which write through the XCD's L2;
+//      after they complete, the workgroup bumps the segment's counter.  The
+//      workgroup that completes the count reads every piece of the segment with
 //      device-scope loads, merges them in piece order with log-sum-exp weights,
 //      writes the output and resets the counter.  No workgroup waits for another,
 //      and no device-scope fence (a whole-L2 writeback and invalidate per XCD) is
@@ -52,9 +57,14 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 #ifndef RLDA_MFMA_DEPTH
 #define RLDA_MFMA_DEPTH 3                    // pages in flight per wave, MFMA path
 #endif
+#ifndef RLDA_MFMA_DEPTH_FP8
+#define RLDA_MFMA_DEPTH_FP8 RLDA_MFMA_DEPTH  // ... with fp8 pages (half the bytes each)
+#endif
+constexpr float kRescaleLog2 = 8.f;          // see Mfma::compute
 constexpr int kChunk = 64;                   // page ids fetched per vector load
 constexpr uint32_t kRsrcWord3 = 0x00020000u; // raw buffer, 32-bit data format
 constexpr int kLoadNT = 2;                   // cache policy: non-temporal (KV is read once)
+constexpr int kPastRange = 0x40000000;       // buffer offset beyond any descriptor's records: reads 0
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_huge_valf(); }
 
@@ -69,6 +79,12 @@ __device__ __forceinline__ int64_t uni64(int64_t x) {
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, (int)kRsrcWord3);
+}
+
+// Descriptor from wave-uniform inputs, kept in scalar registers.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc_uni(const void* base, uint32_t bytes) {
+  const int64_t a = uni64((int64_t)(uintptr_t)base);
+  return make_rsrc((const void*)(uintptr_t)a, (uint32_t)uni((int)bytes));
 }
 
 template <int BYTES>
@@ -147,6 +163,10 @@ __device__ __forceinline__ void store_out(const Params& p, int b, int qh, int d0
   store_row<D, D / 16>(p, b, qh, d0, o, inv);
 }
 
+// Query heads of each KV head (a copy of Params::q_head, filled at kernel start):
+// s_qhead[g * G + i] is the i-th query head of KV head g.
+__shared__ int16_t s_qhead[kMaxQHeads];
+
 // Device-scope (sc1) store / load: coherent across XCDs without L2 maintenance.
 __device__ __forceinline__ void store_device(float* p, float v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -183,7 +203,7 @@ __device__ __forceinline__ void merge_pieces(const Params& p, int b, int g, int 
     for (int e = 0; e < DPT; ++e) o[e] = o[e] * a_old + v[e] * a_new;
     M = Mn;
   }
-  store_out<D>(p, b, p.q_head[g * G + h], d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
+  store_out<D>(p, b, s_qhead[g * G + h], d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
 }
 
 // ---------------------------------------------------------------- MFMA policy
@@ -202,7 +222,7 @@ struct Mfma {
   static constexpr int DT = D / 16;                  // output tiles = V elements per row per lane
   static constexpr int EB = FP8 ? 1 : 2;             // bytes per KV element
   static constexpr int kEB = EB;
-  static constexpr int kDepth = RLDA_MFMA_DEPTH;
+  static constexpr int kDepth = FP8 ? RLDA_MFMA_DEPTH_FP8 : RLDA_MFMA_DEPTH;
   static constexpr int KL = FP8 ? D / 64 : D / 32;   // 16-byte K loads per lane
   static constexpr int VB = DT * EB;                 // V bytes per row per lane
   typedef typename RowLoad<VB>::type VRow;
@@ -212,34 +232,53 @@ struct Mfma {
     VRow v[4];
   };
 
+  // Q operand of one (sequence, KV head): lane 16q+i holds head i's chunks for the k-steps.
+  struct QOp {
+    bf16x8 v[KS];
+  };
+  static constexpr bool kQRing = true;   // the Q operand travels with the pages in flight
+
   f32x4 acc[DT];
   float m, l;
-  bf16x8 q[KS];
-  int koff[KL], voff[4];
+  QOp q;
+  int koff[KL], voff[4], qoff[KS];
 
   __device__ __forceinline__ static int chunk_of(int qg, int s) {
     return FP8 ? 8 * (s >> 1) + 2 * qg + (s & 1) : 4 * s + qg;
   }
 
-  __device__ __forceinline__ void init(const Params& p, int b, int g, int lane, int32_t ss) {
+  __device__ __forceinline__ void setup(const Params& p, int lane, int32_t ss) {
     const int i = lane & 15, qg = lane >> 4;
-#pragma unroll
-    for (int t = 0; t < DT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    m = neg_inf();
-    l = 0.f;
-    const int G = p.group;
-    const uint16_t* qb = nullptr;
-    if (i < G) qb = (const uint16_t*)p.q + ((int64_t)b * p.num_q_heads + p.q_head[g * G + i]) * D;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      u32x4 w = {0u, 0u, 0u, 0u};
-      if (qb) w = *(const u32x4*)(qb + 8 * chunk_of(qg, s));
-      q[s] = __builtin_bit_cast(bf16x8, w);
-    }
 #pragma unroll
     for (int s = 0; s < KL; ++s) koff[s] = i * ss + (FP8 ? 64 * s + 16 * qg : 16 * chunk_of(qg, s));
 #pragma unroll
     for (int r = 0; r < 4; ++r) voff[r] = (4 * qg + r) * ss + i * VB;
+    (void)p;
+  }
+
+  // Q rows of KV head g of sequence b, issued (when `load`) together with the
+  // first page of the segment.  Padding rows (i >= G) read past the descriptor's
+  // range and get zeros, so no instruction touches the loaded values before they
+  // are consumed and the loads stay in flight with the page's.
+  __device__ __forceinline__ static void load_q(QOp& qo, const Params& p, int b, int g, int lane, bool load) {
+    if (!load) return;
+    const int i = lane & 15, qg = lane >> 4;
+    const int G = p.group;
+    const uint16_t* qb = (const uint16_t*)p.q + (int64_t)b * p.num_q_heads * D;
+    const __amdgpu_buffer_rsrc_t r = make_rsrc_uni(qb, load ? (uint32_t)(p.num_q_heads * D * 2) : 0u);
+    const int row = (i < G) ? s_qhead[g * G + i] * D * 2 : kPastRange;
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      qo.v[s] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, row + 16 * chunk_of(qg, s), 0, 0));
+  }
+
+  // Start accumulating a new (sequence, KV head) with its Q operand.
+  __device__ __forceinline__ void begin(const QOp& qo, const Params&, int, int, int) {
+#pragma unroll
+    for (int t = 0; t < DT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m = neg_inf();
+    l = 0.f;
+    q = qo;
   }
 
   __device__ __forceinline__ void issue(Frag& f, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv) const {
@@ -269,7 +308,7 @@ struct Mfma {
     const int qg = lane >> 4;
     f32x4 sc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int s = 0; s < KS; ++s) sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand(f, s), q[s], sc, 0, 0, 0);
+    for (int s = 0; s < KS; ++s) sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand(f, s), q.v[s], sc, 0, 0, 0);
     float sv[4];
     float mx = neg_inf();
 #pragma unroll
@@ -278,9 +317,21 @@ struct Mfma {
       mx = fmaxf(mx, sv[r]);
     }
     mx = group_max(mx);
-    const float mn = fmaxf(m, mx);
-    const float mu = (mn == neg_inf()) ? 0.f : mn;
-    const float alpha = __builtin_amdgcn_exp2f(m - mu);
+    // The reference maximum m only moves when a score exceeds it by more than
+    // 2^kRescaleLog2: probabilities stay <= 2^kRescaleLog2 (exact in fp32, the
+    // same relative rounding in bf16), and the accumulator rescale, which reads
+    // and writes every accumulator register, is skipped on almost every page.
+    const bool up = mx > m + kRescaleLog2;   // always when m is still -inf and mx is not
+    if (__builtin_amdgcn_ballot_w64(up) != 0)
+    {
+      const float mn = up ? mx : m;
+      const float alpha = __builtin_amdgcn_exp2f(m - mn);   // 0 from -inf, 1 when unchanged
+      l *= alpha;
+      m = mn;
+#pragma unroll
+      for (int t = 0; t < DT; ++t) acc[t] *= alpha;
+    }
+    const float mu = (m == neg_inf()) ? 0.f : m;
     float pr[4];
     float ps = 0.f;
 #pragma unroll
@@ -288,10 +339,7 @@ struct Mfma {
       pr[r] = __builtin_amdgcn_exp2f(sv[r] - mu);
       ps += pr[r];
     }
-    l = l * alpha + ps;
-    m = mn;
-#pragma unroll
-    for (int t = 0; t < DT; ++t) acc[t] *= alpha;
+    l += ps;
     u32x2 pb2 = {pack_bf16(pr[0] * vmul, pr[1] * vmul), pack_bf16(pr[2] * vmul, pr[3] * vmul)};
     const s16x4 pb = __builtin_bit_cast(s16x4, pb2);
     if constexpr (!FP8) {
@@ -352,7 +400,7 @@ struct Mfma {
     for (int r = 0; r < 4; ++r)
 #pragma unroll
       for (int t = 0; t < DT; ++t) o[r * DT + t] = acc[t][r];
-    store_row<D, 4 * DT>(p, b, p.q_head[g * p.group + i], 4 * DT * qg, o, lt > 0.f ? 1.f / lt : 0.f);
+    store_row<D, 4 * DT>(p, b, s_qhead[g * p.group + i], 4 * DT * qg, o, lt > 0.f ? 1.f / lt : 0.f);
   }
 };
 
@@ -370,27 +418,35 @@ struct Valu {
     u32x4 k[NL];
     u32x4 v[NL];
   };
+  struct QOp {};
+  static constexpr bool kQRing = false;   // q is loaded when a segment begins
+
   float acc[GM][CW];
   float qv[GM][CW];
   float m[GM], l[GM];
   int off;
 
-  __device__ __forceinline__ void init(const Params& p, int b, int g, int lane, int32_t ss) {
-    const int t = lane >> 2, c = lane & 3;
+  __device__ __forceinline__ void setup(const Params&, int lane, int32_t ss) {
+    off = (lane >> 2) * ss + (lane & 3) * CW * 4;
+  }
+
+  __device__ __forceinline__ static void load_q(QOp&, const Params&, int, int, int, bool) {}
+
+  __device__ __forceinline__ void begin(const QOp&, const Params& p, int b, int g, int lane) {
+    const int c = lane & 3;
     const int G = p.group;
 #pragma unroll
     for (int h = 0; h < GM; ++h) {
       m[h] = neg_inf();
       l[h] = 0.f;
       const float* qb = nullptr;
-      if (h < G) qb = (const float*)p.q + ((int64_t)b * p.num_q_heads + p.q_head[g * G + h]) * D + c * CW;
+      if (h < G) qb = (const float*)p.q + ((int64_t)b * p.num_q_heads + s_qhead[g * G + h]) * D + c * CW;
 #pragma unroll
       for (int j = 0; j < CW; ++j) {
         acc[h][j] = 0.f;
         qv[h][j] = qb ? qb[j] : 0.f;
       }
     }
-    off = t * ss + c * CW * 4;
   }
 
   __device__ __forceinline__ void issue(Frag& f, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv) const {
@@ -467,9 +523,52 @@ struct Valu {
     if (lane >= 4) return;
 #pragma unroll
     for (int h = 0; h < GM; ++h)
-      if (h < p.group) store_row<D, CW>(p, b, p.q_head[g * p.group + h], c * CW, acc[h], lt[h] > 0.f ? 1.f / lt[h] : 0.f);
+      if (h < p.group) store_row<D, CW>(p, b, s_qhead[g * p.group + h], c * CW, acc[h], lt[h] > 0.f ? 1.f / lt[h] : 0.f);
   }
 };
+
+// ---------------------------------------------------------------- stream metadata
+// A wave walks its quarter [w0, w1) of the flattened (sequence, KV head, page) list
+// as one continuous page stream.  Its lanes describe 64 consecutive positions at a
+// time (lane k: position base + k), fetched one chunk ahead of use.
+constexpr int kInfoTok = 31;            // valid tokens of the page (0: nothing to read)
+constexpr int kInfoFirst = 1 << 5;      // first page of its (sequence, KV head)
+constexpr int kInfoLast = 1 << 6;       // last page of its (sequence, KV head)
+constexpr int kInfoStart = 1 << 7;      // first position of this wave's quarter
+constexpr int kInfoEnd = 1 << 8;        // last position of this wave's quarter
+constexpr int kInfoHeadShift = 9;       // KV head g: 8 bits
+constexpr int kInfoSeqShift = 17;       // sequence b: up to 14 bits
+
+// The page id is returned as read; it is checked where it is used, so that
+// nothing waits for these loads until the chunk is consumed.
+struct StreamChunk {
+  int pid;      // page id from the block table (lanes past the quarter: -1)
+  int info;     // bits above
+};
+
+// Positions fit in 32 bits: the host rejects max_batch * max_pages * Hkv >= 2^31.
+__device__ __forceinline__ StreamChunk fetch_chunk(const Params& p, const int32_t* s_pre, const uint8_t* s_tail,
+                                                   int base, int w0, int w1, int lane) {
+  StreamChunk c = {-1, 0};
+  const int pos = base + lane;
+  if (pos < w1) {
+    const int Hkv = p.num_kv_heads;
+    const int y = (int)((uint32_t)pos / (uint32_t)Hkv);
+    int lo = 0, hi = p.batch;   // s_pre[lo] <= y < s_pre[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (s_pre[mid] <= y) lo = mid; else hi = mid;
+    }
+    const int b = lo, pre = s_pre[b], nb = s_pre[b + 1] - pre;
+    const int off = pos - Hkv * pre;
+    const int g = (int)((uint32_t)off / (uint32_t)nb), j = off - g * nb;
+    const int tok = (j == nb - 1) ? s_tail[b] : kPage;
+    c.pid = p.block_table[(int64_t)b * p.max_pages + j];
+    c.info = tok | (j == 0 ? kInfoFirst : 0) | (j == nb - 1 ? kInfoLast : 0) | (pos == w0 ? kInfoStart : 0) |
+             (pos == w1 - 1 ? kInfoEnd : 0) | (g << kInfoHeadShift) | (b << kInfoSeqShift);
+  }
+  return c;
+}
 
 // ---------------------------------------------------------------- the kernel
 
@@ -479,6 +578,7 @@ void decode_attention_kernel(const Params p) {
   constexpr int D = Pol::kD;
   constexpr int DPT = D / 16;   // output elements per thread in the workgroup merge
   __shared__ int32_t s_pre[kMaxBatch + 1];
+  __shared__ uint8_t s_tail[kMaxBatch];   // valid tokens of each sequence's last page
   // Cut pieces: slot 2w holds wave w's piece that began before its quarter of the
   // share, slot 2w+1 its piece that continues past it.
   __shared__ float s_acc[2 * kWaves][16][D + 4];
@@ -503,6 +603,7 @@ void decode_attention_kernel(const Params p) {
       L = min(max(L, 0), cap);
       const int n = (L + kPage - 1) / kPage;
       s_pre[b + 1] = n;
+      s_tail[b] = (uint8_t)(L - (n - 1) * kPage);   // 1..16 when n > 0
       sum += n;
     }
     if (bad && u == 0) atomicOr(p.flags, kFlagBadLen);
@@ -513,6 +614,7 @@ void decode_attention_kernel(const Params p) {
       if (lane >= o) x += y;
     }
     if (lane == 63) s_scan[wave] = x;
+    for (int e = tid; e < p.num_q_heads; e += kThreads) s_qhead[e] = p.q_head[e];
     if (tid < 2 * kWaves) s_seg[tid] = -1;
     __syncthreads();
     int run = x - sum;
@@ -547,87 +649,86 @@ void decode_attention_kernel(const Params p) {
   //    pieces without waiting for the others; a piece inside its quarter is
   //    written directly.
   const int64_t r0 = (int64_t)u * T / Wn, r1 = (int64_t)(u + 1) * T / Wn;
-  const int64_t w0 = r0 + (r1 - r0) * wave / kWaves, w1 = r0 + (r1 - r0) * (wave + 1) / kWaves;
-  int64_t x = w0;
-  while (x < w1) {
-    int lo = 0, hi = batch;   // s_pre[lo] <= y < s_pre[hi]
-    {
-      const int64_t y = x / Hkv;
-      while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (s_pre[mid] <= y) lo = mid; else hi = mid;
-      }
-    }
-    const int b = uni(lo);
-    const int pre_b = uni(s_pre[b]);
-    const int nb = uni(s_pre[b + 1]) - pre_b;
-    const int64_t off = x - (int64_t)Hkv * pre_b;
-    const int g = (int)(off / nb);
-    const int j0 = (int)(off % nb);
-    const int64_t seg_end = x - j0 + nb;
-    const int64_t pe = min(w1, seg_end);
-    const int j1 = j0 + (int)(pe - x);
-    const int len = min(max(p.seq_lens[b], 0), cap);
-
+  const int w0 = (int)(r0 + (r1 - r0) * wave / kWaves), w1 = (int)(r0 + (r1 - r0) * (wave + 1) / kWaves);
+  if (w0 < w1) {
+    constexpr int kDepth = Pol::kDepth;
     Pol st;
-    st.init(p, b, g, lane, p.stride_slot);
-    const char* kg = (const char*)p.k + (int64_t)g * p.stride_head;
-    const char* vg = (const char*)p.v + (int64_t)g * p.stride_head;
-    for (int cb = j0; cb < j1; cb += kChunk) {
-      const int cn = min(kChunk, j1 - cb);
-      int pid = p.block_table[(int64_t)b * p.max_pages + cb + min(lane, cn - 1)];
-      if ((unsigned)pid >= (unsigned)p.num_pages) {
-        atomicOr(p.flags, kFlagBadPage);
-        pid = -1;
-      }
-      float ksc = 1.f, vsc = 1.f;
-      if constexpr (Pol::kFp8) {
-        ksc = pid >= 0 ? p.k_scale[(int64_t)pid * Hkv + g] : 0.f;
-        vsc = pid >= 0 ? p.v_scale[(int64_t)pid * Hkv + g] : 0.f;
-      }
-      constexpr int kDepth = Pol::kDepth;
+    st.setup(p, lane, p.stride_slot);
+    typename Pol::QOp qring[kDepth];
+    bool began = false;   // the segment being accumulated began inside this quarter
+    StreamChunk nxt = fetch_chunk(p, s_pre, s_tail, w0, w0, w1, lane);
+    for (int base = w0; base < w1; base += kChunk) {
+      const StreamChunk cur = nxt;
+      const int cn = min(kChunk, w1 - base);
+      if (base + kChunk < w1) nxt = fetch_chunk(p, s_pre, s_tail, base + kChunk, w0, w1, lane);
       typename Pol::Frag fr[kDepth];
-      auto issue = [&](typename Pol::Frag& f, int k) {
-        int pk = -1;
-        if (k < cn) pk = __builtin_amdgcn_readlane(pid, k);
-        const int rows = (pk >= 0) ? min(kPage, len - (cb + k) * kPage) : 0;
-        const int64_t po = (pk >= 0) ? (int64_t)pk * p.stride_page : 0;
-        const uint32_t nrec = rows > 0 ? (uint32_t)((rows - 1) * p.stride_slot + D * Pol::kEB) : 0u;
-        st.issue(f, make_rsrc(kg + po, nrec), make_rsrc(vg + po, nrec));
-      };
-      auto compute = [&](const typename Pol::Frag& f, int k) {
-        int valid = 0;
-        float km = p.scale_log2, vm = 1.f;
+      int sinfo[kDepth];
+      float skm[kDepth], svm[kDepth];
+      // Issue the loads of position base + k into pipeline slot `sl`.
+      auto issue = [&](typename Pol::Frag& f, int& info_out, float& km_out, float& vm_out,
+                       typename Pol::QOp& q_out, int k) {
+        // Past the chunk the descriptors have no records: the loads still issue (so
+        // every path through the loop issues the same loads) but read nothing.
+        int pk = -1, info = 0;
+        float ks = 1.f, vs = 1.f;
         if (k < cn) {
-          const int pk = __builtin_amdgcn_readlane(pid, k);
-          valid = (pk >= 0) ? len - (cb + k) * kPage : 0;
-          if constexpr (Pol::kFp8) {
-            km *= __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ksc), k));
-            vm = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, vsc), k));
+          pk = __builtin_amdgcn_readlane(cur.pid, k);
+          info = __builtin_amdgcn_readlane(cur.info, k);
+          if ((unsigned)pk >= (unsigned)p.num_pages) {   // not a page of the pool: contributes nothing
+            if (lane == 0) atomicOr(p.flags, kFlagBadPage);
+            pk = -1;
+            info &= ~kInfoTok;
           }
         }
-        st.compute(f, lane, valid, km, vm);
+        const int tok = info & kInfoTok;
+        const int g = (info >> kInfoHeadShift) & 255, b = info >> kInfoSeqShift;
+        if constexpr (Pol::kFp8) {
+          // Scales of (page, KV head); no records (reads of zero) for an absent page.
+          const int64_t si = (pk >= 0) ? (int64_t)pk * Hkv + g : 0;
+          const uint32_t sb = (pk >= 0) ? 4u : 0u;
+          ks = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(make_rsrc_uni(p.k_scale + si, sb), 0, 0, 0));
+          vs = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(make_rsrc_uni(p.v_scale + si, sb), 0, 0, 0));
+        }
+        const int64_t po = (pk >= 0) ? (int64_t)pk * p.stride_page + (int64_t)g * p.stride_head : 0;
+        const uint32_t nrec = tok > 0 ? (uint32_t)((tok - 1) * p.stride_slot + D * Pol::kEB) : 0u;
+        st.issue(f, make_rsrc_uni((const char*)p.k + po, nrec), make_rsrc_uni((const char*)p.v + po, nrec));
+        if constexpr (Pol::kQRing) Pol::load_q(q_out, p, b, g, lane, (info & (kInfoFirst | kInfoStart)) != 0);
+        info_out = info;   // the scales are used as loaded, in compute
+        km_out = ks;
+        vm_out = vs;
+      };
+      // Consume pipeline slot `sl` (position base + k).
+      auto compute = [&](const typename Pol::Frag& f, int info, float km, float vm, const typename Pol::QOp& q,
+                         int k) {
+        if (k >= cn) return;
+        const int g = (info >> kInfoHeadShift) & 255, b = info >> kInfoSeqShift;
+        if (info & (kInfoFirst | kInfoStart)) {
+          st.begin(q, p, b, g, lane);
+          began = (info & kInfoFirst) != 0;
+        }
+        st.compute(f, lane, info & kInfoTok, p.scale_log2 * km, vm);
+        if (info & (kInfoLast | kInfoEnd)) {
+          const bool ended = (info & kInfoLast) != 0;
+          if (began && ended) {
+            st.write_out(p, b, g, lane);
+          } else {
+            const int slot = 2 * wave + (ended ? 0 : 1);
+            st.to_lds(s_acc[slot], s_ml[slot], lane);
+            if (lane == 0) s_seg[slot] = b * Hkv + g;
+          }
+        }
       };
 #pragma unroll
-      for (int k = 0; k < kDepth - 1; ++k) issue(fr[k], k);
+      for (int k = 0; k < kDepth - 1; ++k) issue(fr[k], sinfo[k], skm[k], svm[k], qring[k], k);
       for (int i = 0; i < cn; i += kDepth) {
 #pragma unroll
         for (int k = 0; k < kDepth; ++k) {
-          issue(fr[(k + kDepth - 1) % kDepth], i + k + kDepth - 1);
-          compute(fr[k], i + k);
+          const int si = (k + kDepth - 1) % kDepth;
+          issue(fr[si], sinfo[si], skm[si], svm[si], qring[si], i + k + kDepth - 1);
+          compute(fr[k], sinfo[k], skm[k], svm[k], qring[k], i + k);
         }
       }
     }
-    const bool before = j0 > 0;            // the segment began before this quarter
-    const bool after = pe < seg_end;       // ... or continues past it
-    if (!before && !after) {
-      st.write_out(p, b, g, lane);
-    } else {
-      const int slot = 2 * wave + (after ? 1 : 0);
-      st.to_lds(s_acc[slot], s_ml[slot], lane);
-      if (lane == 0) s_seg[slot] = b * Hkv + g;
-    }
-    x = pe;
   }
   __syncthreads();
 
@@ -666,7 +767,7 @@ void decode_attention_kernel(const Params p) {
         for (int e = 0; e < DPT; ++e) o[e] += a * s_acc[j][h][d0 + e];
       }
       if (whole) {
-        store_out<D>(p, b, p.q_head[g * G + h], d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
+        store_out<D>(p, b, s_qhead[g * G + h], d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
       } else {
         const int64_t gs = (seg_end > r1) ? 2 * (int64_t)u + 1 : 2 * (int64_t)u;
         float* dst = p.part_acc + (gs * G + h) * D + d0;

@@ -78,6 +78,7 @@ def test_create_accepts_the_workload_configurations(lib):
     (dict(kv_stride_page=1001 * 8, kv_stride_head=2048, kv_stride_slot=132), -1),      # row not 16-B aligned
     (dict(softmax_scale=-1.0), -1),
     (dict(num_work_ranges=5000), -1),
+    (dict(max_batch=8192, max_pages_per_seq=65536, num_kv_heads=4, num_q_heads=28), -2),   # > 2^31 units
 ])
 def test_create_rejects_bad_configurations(lib, kw, want):
     st, h = create(lib, cfg(**kw))

@@ -153,6 +153,46 @@ def test_shared_prefix_group(torch_cuda):
     assert_close(got, oracle.run(w), "bf16", "prefix")
 
 
+def steer_scores(w, slope, seed=5):
+    """Replace q and the valid K rows so that token t of every sequence scores about
+    `slope * t / 16` (log2 units) against every query head: q = 8u + noise and
+    K_t = (slope * t / 16) u + noise with a unit vector u per KV head.  Unused slots
+    and pages keep their NaN poison."""
+    import dataclasses
+    rng = np.random.default_rng(seed)
+    d = w.head_dim
+    u = rng.standard_normal((w.num_kv_heads, d))
+    u /= np.linalg.norm(u, axis=1, keepdims=True)
+    # softmax_scale * log2(e) * 8 |u|^2 * c = c  (log2 units per unit of c)
+    a = 1.0 / (8.0 / np.sqrt(d) * np.log2(np.e))
+    qf = I.bf16_bits_to_f32(w.q).astype(np.float64)
+    for h in range(w.num_q_heads):
+        qf[:, h] = 8.0 * u[w.kv_head_of_q[h]] + 0.05 * qf[:, h]
+    kf = I.bf16_bits_to_f32(w.k_cache).astype(np.float64)   # [NP][Hkv][P][d]
+    for b in range(w.batch):
+        L = int(w.seq_lens[b])
+        n = (L + 15) // 16
+        for j in range(n):
+            pid = int(w.block_table[b, j])
+            rows = min(16, L - 16 * j)
+            c = a * slope * (16 * j + np.arange(rows)) / 16.0
+            kf[pid, :, :rows] = c[None, :, None] * u[:, None, :] + 0.05 * kf[pid, :, :rows]
+    return dataclasses.replace(w, q=I.f32_to_bf16_bits(qf.astype(np.float32)),
+                               k_cache=I.f32_to_bf16_bits(kf.astype(np.float32)))
+
+
+@pytest.mark.parametrize("slope", [1.0, 20.0, -1.0, 0.37])
+def test_rising_and_falling_scores(torch_cuda, slope):
+    """Scores that climb slowly (the reference max moves every ~8 pages, so
+    probabilities up to 2^8 reach the PV product), steeply (it moves on every
+    page), fall (it never moves after the first page) or drift."""
+    w = steer_scores(I.make_custom([2000, 1000, 37, 513, 16, 1], 28, 4, 128, seed=31), slope)
+    want = oracle.run(w)
+    for ranges in (0, 7):
+        got, _ = gpu_run(torch_cuda, w, ranges=ranges, tag=f"slope={slope}")
+        assert_close(got, want, "bf16", f"slope={slope} ranges={ranges}")
+
+
 def test_repeated_runs_are_bitwise_deterministic(torch_cuda):
     torch = torch_cuda
     w = I.make_custom([3000, 20, 1700, 9, 800], 28, 4, 128, q_dtype="bf16", kv_dtype="bf16", seed=13)
