@@ -588,7 +588,15 @@ void decode_attention_kernel(const Params p) {
   __shared__ int32_t s_last[2];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
-  const int u = blockIdx.x, W = p.nranges;
+  const int W = p.nranges;
+  // Share index.  Workgroups are dispatched round-robin over the 8 XCDs (block b
+  // runs on XCD b % 8); each XCD gets a contiguous run of shares, so neighbouring
+  // work (the sequences of a GRPO group reading the same prompt pages, the pieces
+  // of one split segment) shares one L2.  A bijection of [0, W).
+  const int u = [&] {
+    const int b = blockIdx.x, x = b & 7, i = b >> 3, q = W >> 3, r = W & 7;
+    return x * q + min(x, r) + i;
+  }();
   const int batch = p.batch, Hkv = p.num_kv_heads, G = p.group;
   const int cap = p.max_pages * kPage;
 
@@ -667,8 +675,6 @@ void decode_attention_kernel(const Params p) {
       // Issue the loads of position base + k into pipeline slot `sl`.
       auto issue = [&](typename Pol::Frag& f, int& info_out, float& km_out, float& vm_out,
                        typename Pol::QOp& q_out, int k) {
-        // Past the chunk the descriptors have no records: the loads still issue (so
-        // every path through the loop issues the same loads) but read nothing.
         int pk = -1, info = 0;
         float ks = 1.f, vs = 1.f;
         if (k < cn) {
@@ -719,12 +725,24 @@ void decode_attention_kernel(const Params p) {
         }
       };
 #pragma unroll
-      for (int k = 0; k < kDepth - 1; ++k) issue(fr[k], sinfo[k], skm[k], svm[k], qring[k], k);
-      for (int i = 0; i < cn; i += kDepth) {
+      for (int k = 0; k < kDepth - 1; ++k)
+        if (k < cn) issue(fr[k], sinfo[k], skm[k], svm[k], qring[k], k);
+      int i = 0;
+      // Steady state: every position issued lies inside the chunk.
+      for (; i + 2 * kDepth - 2 < cn; i += kDepth) {
 #pragma unroll
         for (int k = 0; k < kDepth; ++k) {
           const int si = (k + kDepth - 1) % kDepth;
           issue(fr[si], sinfo[si], skm[si], svm[si], qring[si], i + k + kDepth - 1);
+          compute(fr[k], sinfo[k], skm[k], svm[k], qring[k], i + k);
+        }
+      }
+      // Drain: no loads are issued past the chunk, so none is left in flight.
+      for (; i < cn; i += kDepth) {
+#pragma unroll
+        for (int k = 0; k < kDepth; ++k) {
+          const int si = (k + kDepth - 1) % kDepth;
+          if (i + k + kDepth - 1 < cn) issue(fr[si], sinfo[si], skm[si], svm[si], qring[si], i + k + kDepth - 1);
           compute(fr[k], sinfo[k], skm[k], svm[k], qring[k], i + k);
         }
       }

@@ -90,3 +90,16 @@ def test_each_share_holds_equal_work():
     for p in pieces:
         per[p["u"]] += p["j1"] - p["j0"]
     assert per.max() - per.min() <= 1
+
+
+@pytest.mark.parametrize("W", list(range(1, 70)) + [255, 256, 257, 1024, 4095, 4096])
+def test_xcd_share_map_is_a_bijection_with_contiguous_runs(W):
+    """Block b runs on XCD b % 8 and takes share x*q + min(x, r) + b // 8 (x = b % 8,
+    q = W // 8, r = W % 8): every share is taken once and each XCD's shares are one
+    contiguous run."""
+    q, r = W // 8, W % 8
+    share = [(b % 8) * q + min(b % 8, r) + b // 8 for b in range(W)]
+    assert sorted(share) == list(range(W))
+    for x in range(8):
+        mine = sorted(s for b, s in enumerate(share) if b % 8 == x)
+        assert mine == list(range(mine[0], mine[0] + len(mine))) if mine else True
