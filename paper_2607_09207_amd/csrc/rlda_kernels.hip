@@ -167,41 +167,64 @@ __device__ __forceinline__ void store_out(const Params& p, int b, int qh, int d0
 // s_qhead[g * G + i] is the i-th query head of KV head g.
 __shared__ int16_t s_qhead[kMaxQHeads];
 
-// Device-scope (sc1) store / load: coherent across XCDs without L2 maintenance.
-__device__ __forceinline__ void store_device(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float load_device(const float* p) {
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Partials of split segments live in the workspace: slot sl of query row h holds
+// (m, l) at part_ml[(sl*G + h)*2] and the unnormalised output at
+// part_acc[(sl*G + h)*D ...], sl < 2*nranges.  They are written and read with the
+// sc1 cache policy (device scope: write-through past the XCD's L2 and read from
+// the coherent level), so workgroups on different XCDs exchange them without L2
+// writeback or invalidate.
+constexpr int kDeviceScope = 16;             // buffer cache-policy bit sc1
+struct PartialRsrc {
+  __amdgpu_buffer_rsrc_t acc, ml;
+  template <int D>
+  __device__ __forceinline__ static PartialRsrc of(const Params& p) {
+    const uint32_t slots = 2u * (uint32_t)p.nranges * (uint32_t)p.group;
+    return {make_rsrc_uni(p.part_acc, slots * D * 4u), make_rsrc_uni(p.part_ml, slots * 8u)};
+  }
+};
+
+// Online log-sum-exp merge of one partial (mj, lj, v[]) into (M, Ls, o[]).
+template <int N>
+__device__ __forceinline__ void lse_merge(float& M, float& Ls, float* o, float mj, float lj, const float* v) {
+  if (mj == neg_inf()) return;
+  const float Mn = fmaxf(M, mj);
+  const float a_old = __builtin_amdgcn_exp2f(M - Mn), a_new = __builtin_amdgcn_exp2f(mj - Mn);
+  Ls = Ls * a_old + lj * a_new;
+#pragma unroll
+  for (int e = 0; e < N; ++e) o[e] = o[e] * a_old + v[e] * a_new;
+  M = Mn;
 }
 
 // Merge the pieces of segment (b, g) held by workgroups u_first..u_last: the piece
 // of workgroup k is in slot 2k+1 when it continues past k's share, else in slot 2k.
-// One pass in piece order with a running maximum.  Thread (h, d0) writes its
-// D/16 outputs.
+// Loads are issued kBatch pieces at a time (one round trip per batch), then merged
+// in piece order with a running maximum.  Thread (h, d0) writes its D/16 outputs.
 template <int D>
 __device__ __forceinline__ void merge_pieces(const Params& p, int b, int g, int h, int d0, int64_t u_first,
                                              int64_t u_last) {
-  constexpr int DPT = D / 16;
+  constexpr int DPT = D / 16, kBatch = 4;
   const int G = p.group;
+  const PartialRsrc rs = PartialRsrc::of<D>(p);
   float M = neg_inf(), Ls = 0.f, o[DPT];
 #pragma unroll
   for (int e = 0; e < DPT; ++e) o[e] = 0.f;
-#pragma unroll 2
-  for (int64_t k = u_first; k <= u_last; ++k) {
-    const int64_t sl = (k < u_last) ? 2 * k + 1 : 2 * k;
-    const float mk = load_device(p.part_ml + (sl * G + h) * 2);
-    const float lk = load_device(p.part_ml + (sl * G + h) * 2 + 1);
-    float v[DPT];
+  for (int64_t k0 = u_first; k0 <= u_last; k0 += kBatch) {
+    u32x2 ml[kBatch];
+    float v[kBatch][DPT];
 #pragma unroll
-    for (int e = 0; e < DPT; ++e) v[e] = load_device(p.part_acc + (sl * G + h) * D + d0 + e);
-    if (mk == neg_inf()) continue;
-    const float Mn = fmaxf(M, mk);
-    const float a_old = __builtin_amdgcn_exp2f(M - Mn), a_new = __builtin_amdgcn_exp2f(mk - Mn);
-    Ls = Ls * a_old + lk * a_new;
+    for (int i = 0; i < kBatch; ++i) {
+      const int64_t k = min(k0 + i, u_last);   // past the last piece: re-read it, unused
+      const int sl = (int)((k < u_last) ? 2 * k + 1 : 2 * k);
+      ml[i] = __builtin_amdgcn_raw_buffer_load_b64(rs.ml, (sl * G + h) * 8, 0, kDeviceScope);
 #pragma unroll
-    for (int e = 0; e < DPT; ++e) o[e] = o[e] * a_old + v[e] * a_new;
-    M = Mn;
+      for (int c = 0; c < DPT; c += 4)
+        *(u32x4*)&v[i][c] = __builtin_amdgcn_raw_buffer_load_b128(rs.acc, ((sl * G + h) * D + d0 + c) * 4, 0,
+                                                                   kDeviceScope);
+    }
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i)
+      if (k0 + i <= u_last)
+        lse_merge<DPT>(M, Ls, o, __uint_as_float(ml[i][0]), __uint_as_float(ml[i][1]), v[i]);
   }
   store_out<D>(p, b, s_qhead[g * G + h], d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
 }
@@ -581,8 +604,8 @@ void decode_attention_kernel(const Params p) {
   __shared__ uint8_t s_tail[kMaxBatch];   // valid tokens of each sequence's last page
   // Cut pieces: slot 2w holds wave w's piece that began before its quarter of the
   // share, slot 2w+1 its piece that continues past it.
-  __shared__ float s_acc[2 * kWaves][16][D + 4];
-  __shared__ float s_ml[2 * kWaves][16][2];
+  __shared__ __align__(16) float s_acc[2 * kWaves][16][D + 4];
+  __shared__ __align__(16) float s_ml[2 * kWaves][16][2];
   __shared__ int32_t s_seg[2 * kWaves];
   __shared__ int32_t s_scan[kWaves];
   __shared__ int32_t s_last[2];
@@ -757,48 +780,59 @@ void decode_attention_kernel(const Params p) {
   const int h = tid >> 4, d0 = (tid & 15) * DPT;
   int hand_seg[2] = {-1, -1};
   int nhand = 0;
-  for (int k = 0; k < 2 * kWaves;) {
-    const int sgi = s_seg[k];
-    if (sgi < 0) {
-      ++k;
-      continue;
-    }
-    int k1 = k + 1;
-    while (k1 < 2 * kWaves && (s_seg[k1] == sgi || s_seg[k1] < 0)) ++k1;
-    const int b = sgi / Hkv, g = sgi - b * Hkv;
-    const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
-    const int64_t seg_start = (int64_t)Hkv * pre_b + (int64_t)g * nb, seg_end = seg_start + nb;
-    const bool whole = seg_start >= r0 && seg_end <= r1;
-    if (h < G) {
-      float M = neg_inf();
-      for (int j = k; j < k1; ++j)
-        if (s_seg[j] == sgi) M = fmaxf(M, s_ml[j][h][0]);
-      float Ls = 0.f, o[DPT];
+  {
+    int cur = -1;   // segment of the group being merged
+    float M = neg_inf(), Ls = 0.f, o[DPT];
 #pragma unroll
-      for (int e = 0; e < DPT; ++e) o[e] = 0.f;
-      for (int j = k; j < k1; ++j) {
-        if (s_seg[j] != sgi) continue;
-        const float mj = s_ml[j][h][0];
-        const float a = (mj == neg_inf()) ? 0.f : __builtin_amdgcn_exp2f(mj - M);
-        Ls += a * s_ml[j][h][1];
+    for (int e = 0; e < DPT; ++e) o[e] = 0.f;
+    // Close the group of segment `cur`: write it, or publish this workgroup's piece.
+    auto flush = [&]() {
+      const int b = cur / Hkv, g = cur - b * Hkv;
+      const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
+      const int64_t seg_start = (int64_t)Hkv * pre_b + (int64_t)g * nb, seg_end = seg_start + nb;
+      const bool whole = seg_start >= r0 && seg_end <= r1;
+      if (h < G) {
+        if (whole) {
+          store_out<D>(p, b, s_qhead[g * G + h], d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
+        } else {
+          const PartialRsrc rs = PartialRsrc::of<D>(p);
+          const int gs = (seg_end > r1) ? 2 * u + 1 : 2 * u;
 #pragma unroll
-        for (int e = 0; e < DPT; ++e) o[e] += a * s_acc[j][h][d0 + e];
-      }
-      if (whole) {
-        store_out<D>(p, b, s_qhead[g * G + h], d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
-      } else {
-        const int64_t gs = (seg_end > r1) ? 2 * (int64_t)u + 1 : 2 * (int64_t)u;
-        float* dst = p.part_acc + (gs * G + h) * D + d0;
-#pragma unroll
-        for (int e = 0; e < DPT; ++e) store_device(dst + e, o[e]);
-        if ((tid & 15) == 0) {
-          store_device(p.part_ml + (gs * G + h) * 2, M);
-          store_device(p.part_ml + (gs * G + h) * 2 + 1, Ls);
+          for (int c = 0; c < DPT; c += 4)
+            __builtin_amdgcn_raw_buffer_store_b128(*(const u32x4*)&o[c], rs.acc, ((gs * G + h) * D + d0 + c) * 4, 0,
+                                                   kDeviceScope);
+          if ((tid & 15) == 0)
+            __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(M), __float_as_uint(Ls)}, rs.ml,
+                                                  (gs * G + h) * 8, 0, kDeviceScope);
         }
       }
+      if (!whole && nhand < 2) hand_seg[nhand++] = cur;   // only the first and last group can be cut
+    };
+    // Slots in position order; the used slots of one segment are consecutive.  Each
+    // step issues its LDS reads (tag, max/sum, partial output) together.
+#pragma unroll 1
+    for (int j = 0; j <= 2 * kWaves; ++j) {
+      int sj = -2;   // -2: past the last slot
+      float mj = neg_inf(), lj = 0.f, v[DPT];
+      if (j < 2 * kWaves) {
+        sj = s_seg[j];
+        mj = s_ml[j][h][0];
+        lj = s_ml[j][h][1];
+#pragma unroll
+        for (int c = 0; c < DPT; c += 4) *(f32x4*)&v[c] = *(const f32x4*)&s_acc[j][h][d0 + c];
+      }
+      sj = uni(sj);
+      if (sj == -1) continue;   // unused slot
+      if (sj != cur) {
+        if (cur >= 0) flush();
+        cur = sj;
+        M = neg_inf();
+        Ls = 0.f;
+#pragma unroll
+        for (int e = 0; e < DPT; ++e) o[e] = 0.f;
+      }
+      if (sj >= 0 && h < G) lse_merge<DPT>(M, Ls, o, mj, lj, v);
     }
-    if (!whole && nhand < 2) hand_seg[nhand++] = sgi;   // only the first and last group can be cut
-    k = k1;
   }
 
   // 5. Segments cut at the share boundary: count this piece; the workgroup that
