@@ -114,6 +114,10 @@ def main():
     ap.add_argument("--mode", choices=["attention", "copy"], default="attention",
                     help="copy: a plain device copy of --copy-mib MiB, the reference for HBM counter scaling")
     ap.add_argument("--copy-mib", type=int, default=256)
+    ap.add_argument("--prompt-tokens", type=int, default=0,
+                    help="GRPO workload only: prompt length shared by each group (default 512)")
+    ap.add_argument("--grouped", choices=["on", "off"], default="off",
+                    help="on: the shared-prompt entry point (rl_decode_attn_run_grouped) for GRPO workloads")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (this path needs no "
@@ -136,7 +140,12 @@ def main():
         return copy_reference(args, torch, dev)
 
     log(f"generating {args.workload}")
-    w = I.make_workload(args.workload)
+    if args.prompt_tokens:
+        if args.workload != "grpo_shared_prefix_bf16":
+            raise SystemExit("--prompt-tokens applies to grpo_shared_prefix_bf16 only")
+        w = I.grpo_shared_prefix_bf16(prompt_len=args.prompt_tokens)
+    else:
+        w = I.make_workload(args.workload)
     sets = [I.to_torch(w, dev)]
     for _ in range(args.sets - 1):
         s = dict(sets[0])
@@ -148,13 +157,21 @@ def main():
                         w.kv_dtype, "f32", kv_head_of_q=w.kv_head_of_q, kv_strides=strides,
                         num_work_ranges=args.ranges)
     out = torch.empty((w.batch, w.num_q_heads, w.head_dim), dtype=torch.float32, device=dev)
-    ws = h.workspace(dev)
+    grouped = args.grouped == "on"
+    gkw = {}
+    if grouped:
+        if not (w.shared_prefix_tokens > 0 and w.group_size > 1):
+            raise SystemExit(f"--grouped on: workload {w.name} has no shared prompt")
+        ng = (w.batch + w.group_size - 1) // w.group_size
+        gkw = dict(group_size=w.group_size,
+                   prefix_pages=torch.full((ng,), w.shared_prefix_tokens // w.page_size, dtype=torch.int32, device=dev))
+    ws = h.workspace(dev, grouped=grouped)
     stream = torch.cuda.current_stream(dev)
 
     def call(i, events=None):
         s = sets[i % len(sets)]
         h(s["q"], s["k_cache"], s["v_cache"], s["block_table"], s["seq_lens"], k_scale=s["k_scale"],
-          v_scale=s["v_scale"], out=out, workspace=ws, stream=stream, events=events)
+          v_scale=s["v_scale"], out=out, workspace=ws, stream=stream, events=events, **gkw)
 
     log(f"warmup {args.warmup}")
     for i in range(args.warmup):
@@ -220,6 +237,7 @@ def main():
             "hbm_frac": round(value / PEAK_HBM_GBS, 4),
             "sequences_per_s": round(w.batch / (ms_per_step * 1e-3), 1),
             "kv_sets_rotated": len(sets),
+            "shared_prompt_pass": grouped,
         },
         "roofline": {
             "bound": "hbm",

@@ -135,8 +135,47 @@ rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t handle, int32_t batch, 
                                         size_t workspace_bytes, void* stream, void* event_begin,
                                         void* event_end);
 
+/*
+ * Shared-prompt (GRPO group) variant of rl_decode_attn_run.  GRPO samples a group
+ * of responses for each prompt (Sec. 2.1), and every response of a group attends
+ * to the prompt's KV pages.  Sequences [i*group_size, min((i+1)*group_size, batch))
+ * form group i; the first prefix_pages[i] entries of their block-table rows name
+ * the same pool pages (the prompt), each holding page_size valid tokens.  The
+ * result is that of rl_decode_attn_run on the same arguments (up to rounding
+ * order), but each prompt page is read once per KV head for the whole group: a
+ * prompt pass multiplies it against the query rows of up to 64/G members at once
+ * (up to four 16-row MFMA tiles), and the attention over the remaining pages of
+ * each sequence starts from the prompt pass's (max, sum, output) state.
+ *   group_size    >= 1, host value
+ *   prefix_pages  [ceil(batch / group_size)] int32, device memory
+ * The prompt pages are read from the block-table row of the group's first
+ * sequence; the other members' first prefix_pages[i] entries are not read (a
+ * member whose entries differ is computed as if they matched).  A group's prompt
+ * is clamped to the full pages of its shortest member,
+ * min(prefix_pages[i], min over members of floor(seq_lens[b] / 16)), and a clamp
+ * raises flag bit 2; prefix_pages[i] = 0 shares nothing for group i.
+ * Supported for bf16 and fp8 caches (RLDA_ERR_UNSUPPORTED for f32).
+ * workspace: >= rl_decode_attn_grouped_workspace_size bytes, same rules as for
+ * rl_decode_attn_run (the same workspace serves both calls).  Two kernels are
+ * queued on `stream`: the prompt pass, then the attention over the rest.
+ * event_begin / event_end (hipEvent_t): both NULL, or both given to be recorded
+ * before the first and after the second kernel.
+ */
+rlda_status rl_decode_attn_run_grouped(rl_decode_attn_t handle, int32_t batch, int32_t num_pages, int32_t group_size,
+                                       const int32_t* prefix_pages, const void* q, const void* k_cache,
+                                       const void* v_cache, const float* k_scale, const float* v_scale,
+                                       const int32_t* block_table, const int32_t* seq_lens, void* out,
+                                       void* workspace, size_t workspace_bytes, void* stream, void* event_begin,
+                                       void* event_end);
+
+/* Bytes of device workspace rl_decode_attn_run_grouped needs with this handle:
+ * rl_decode_attn_workspace_size plus max_batch*(Hq*(head_dim+2)+1)*4 (rounded up)
+ * for the prompt pass's per-row results (host-only). */
+rlda_status rl_decode_attn_grouped_workspace_size(rl_decode_attn_t handle, size_t* bytes);
+
 /* Flags raised by device-side contract checks since the workspace was zeroed
- * (bit 0: page id outside [0, num_pages); bit 1: seq_len beyond capacity).
+ * (bit 0: page id outside [0, num_pages); bit 1: seq_len beyond capacity;
+ * bit 2: a group's shared prompt clamped to its shortest member).
  * SYNCHRONISES `stream` (waits for queued work, copies 4 bytes to the host). */
 rlda_status rl_decode_attn_read_flags(rl_decode_attn_t handle, const void* workspace, void* stream,
                                       uint32_t* flags);

@@ -68,6 +68,9 @@ class DecodeAttention:
         n = ctypes.c_size_t()
         _abi.check(lib.rl_decode_attn_workspace_size(h, ctypes.byref(n)), "rl_decode_attn_workspace_size")
         self.workspace_bytes = int(n.value)
+        _abi.check(lib.rl_decode_attn_grouped_workspace_size(h, ctypes.byref(n)),
+                   "rl_decode_attn_grouped_workspace_size")
+        self.grouped_workspace_bytes = int(n.value)
         self._ws = {}
 
     def __del__(self):
@@ -76,13 +79,15 @@ class DecodeAttention:
             self._lib.rl_decode_attn_destroy(h)
             self._h = None
 
-    def workspace(self, device):
-        """Zero-filled workspace for `device`, allocated once and reused."""
+    def workspace(self, device, grouped: bool = False):
+        """Zero-filled workspace for `device`, allocated once and reused (grown once
+        for grouped calls, which need more)."""
         torch = _torch()
         key = str(device)
+        need = (self.grouped_workspace_bytes if grouped else self.workspace_bytes) + 256
         ws = self._ws.get(key)
-        if ws is None:
-            ws = torch.zeros(self.workspace_bytes + 256, dtype=torch.uint8, device=device)
+        if ws is None or ws.numel() < need:
+            ws = torch.zeros(need, dtype=torch.uint8, device=device)
             self._ws[key] = ws
         return ws
 
@@ -99,17 +104,21 @@ class DecodeAttention:
         return ev.cuda_event
 
     def __call__(self, q, k_cache, v_cache, block_table, seq_lens, k_scale=None, v_scale=None, out=None,
-                 workspace=None, stream=None, num_pages: Optional[int] = None, events=None):
+                 workspace=None, stream=None, num_pages: Optional[int] = None, events=None,
+                 group_size: Optional[int] = None, prefix_pages=None):
         """Queue the attention on `stream` (default: the current stream).  With
         events=(begin, end) (torch.cuda.Event, timing enabled) the two events bracket
-        the attention kernel itself."""
+        the library's kernels.  With group_size and prefix_pages (int32 device tensor,
+        one entry per group of group_size consecutive sequences) the call shares each
+        group's prompt pages (rl_decode_attn_run_grouped)."""
         torch = _torch()
         B = int(q.shape[0])
         cfg = self.config
         if out is None:
             odt = torch.float32 if cfg.out_dtype == _abi.RLDA_F32 else torch.bfloat16
             out = torch.empty((B, cfg.num_q_heads, cfg.head_dim), dtype=odt, device=q.device)
-        ws = workspace if workspace is not None else self.workspace(q.device)
+        grouped = group_size is not None
+        ws = workspace if workspace is not None else self.workspace(q.device, grouped=grouped)
         if stream is None:
             stream = torch.cuda.current_stream(q.device).cuda_stream
         elif hasattr(stream, "cuda_stream"):
@@ -119,7 +128,11 @@ class DecodeAttention:
         wp = self._aligned_ptr(ws)
         args = (self._h, B, npages, ptr(q), ptr(k_cache), ptr(v_cache), ptr(k_scale), ptr(v_scale),
                 ptr(block_table), ptr(seq_lens), ptr(out), wp, ws.numel() - (wp - ws.data_ptr()), stream)
-        if events is None:
+        if grouped:
+            e0, e1 = (None, None) if events is None else tuple(self._event_handle(e) for e in events)
+            gargs = args[:3] + (int(group_size), ptr(prefix_pages)) + args[3:] + (e0, e1)
+            _abi.check(self._lib.rl_decode_attn_run_grouped(*gargs), "rl_decode_attn_run_grouped")
+        elif events is None:
             _abi.check(self._lib.rl_decode_attn_run(*args), "rl_decode_attn_run")
         else:
             e0, e1 = (self._event_handle(e) for e in events)

@@ -12,8 +12,8 @@ STATUS = {0: "RLDA_OK", -1: "RLDA_ERR_INVALID_ARG", -2: "RLDA_ERR_UNSUPPORTED", 
           -4: "RLDA_ERR_WORKSPACE", -5: "RLDA_ERR_ALLOC"}
 
 EXPORTS = ["rl_decode_attn_create", "rl_decode_attn_workspace_size", "rl_decode_attn_run",
-           "rl_decode_attn_run_profiled", "rl_decode_attn_read_flags", "rl_decode_attn_destroy",
-           "rl_decode_attn_strerror"]
+           "rl_decode_attn_run_profiled", "rl_decode_attn_run_grouped", "rl_decode_attn_grouped_workspace_size",
+           "rl_decode_attn_read_flags", "rl_decode_attn_destroy", "rl_decode_attn_strerror"]
 
 
 class Config(ctypes.Structure):
@@ -62,6 +62,10 @@ def load() -> ctypes.CDLL:
         lib.rl_decode_attn_run.restype = ctypes.c_int
         lib.rl_decode_attn_run_profiled.argtypes = [vp, i32, i32] + [vp] * 8 + [vp, sz, vp, vp, vp]
         lib.rl_decode_attn_run_profiled.restype = ctypes.c_int
+        lib.rl_decode_attn_run_grouped.argtypes = [vp, i32, i32, i32, vp] + [vp] * 8 + [vp, sz, vp, vp, vp]
+        lib.rl_decode_attn_run_grouped.restype = ctypes.c_int
+        lib.rl_decode_attn_grouped_workspace_size.argtypes = [vp, ctypes.POINTER(sz)]
+        lib.rl_decode_attn_grouped_workspace_size.restype = ctypes.c_int
         lib.rl_decode_attn_read_flags.argtypes = [vp, vp, vp, ctypes.POINTER(ctypes.c_uint32)]
         lib.rl_decode_attn_read_flags.restype = ctypes.c_int
         lib.rl_decode_attn_destroy.argtypes = [vp]

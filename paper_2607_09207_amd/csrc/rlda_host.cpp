@@ -33,6 +33,7 @@ int elem_bytes(rlda_dtype t) { return t == RLDA_F32 ? 4 : t == RLDA_BF16 ? 2 : 1
 
 struct WsLayout {
   size_t flags, counters, part_ml, part_acc, total;
+  size_t gprefix, pfx_ml, pfx_acc, grouped_total;   // grouped runs only
 };
 
 WsLayout layout_of(const rlda_handle* h) {
@@ -43,6 +44,10 @@ WsLayout layout_of(const rlda_handle* h) {
   w.part_ml = align_up(w.counters + sizeof(uint32_t) * (size_t)c.max_batch * c.num_kv_heads);
   w.part_acc = align_up(w.part_ml + sizeof(float) * 2 * (size_t)h->ws_ranges * h->group * 2);
   w.total = align_up(w.part_acc + sizeof(float) * 2 * (size_t)h->ws_ranges * h->group * c.head_dim);
+  w.gprefix = w.total;
+  w.pfx_ml = align_up(w.gprefix + sizeof(int32_t) * (size_t)c.max_batch);
+  w.pfx_acc = align_up(w.pfx_ml + sizeof(float) * 2 * (size_t)c.max_batch * c.num_q_heads);
+  w.grouped_total = align_up(w.pfx_acc + sizeof(float) * (size_t)c.max_batch * c.num_q_heads * c.head_dim);
   return w;
 }
 
@@ -144,29 +149,40 @@ rlda_status rl_decode_attn_workspace_size(rl_decode_attn_t h, size_t* bytes) {
   return RLDA_OK;
 }
 
+rlda_status rl_decode_attn_grouped_workspace_size(rl_decode_attn_t h, size_t* bytes) {
+  if (!h || !bytes) return RLDA_ERR_INVALID_ARG;
+  *bytes = layout_of(h).grouped_total;
+  return RLDA_OK;
+}
+
 }  // extern "C"
 
 namespace {
 
-rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, const void* q, const void* k_cache,
-                     const void* v_cache, const float* k_scale, const float* v_scale, const int32_t* block_table,
+// group_size == 0: plain run; > 0: grouped run with prefix_pages.
+rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32_t group_size,
+                     const int32_t* prefix_pages, const void* q, const void* k_cache, const void* v_cache,
+                     const float* k_scale, const float* v_scale, const int32_t* block_table,
                      const int32_t* seq_lens, void* out, void* workspace, size_t workspace_bytes, void* stream,
                      void* ev_begin, void* ev_end) {
   if (!h) return RLDA_ERR_INVALID_ARG;
   const rl_decode_attn_config& c = h->cfg;
-  if (batch < 0 || batch > c.max_batch || num_pages < 0) return RLDA_ERR_INVALID_ARG;
+  const bool grouped = group_size > 0;
+  if (batch < 0 || batch > c.max_batch || num_pages < 0 || group_size < 0) return RLDA_ERR_INVALID_ARG;
+  if (grouped && h->kind == rlda::KvKind::F32) return RLDA_ERR_UNSUPPORTED;
   if (batch == 0) return RLDA_OK;
   if (!q || !block_table || !seq_lens || !out) return RLDA_ERR_INVALID_ARG;
   // An empty pool (every sequence empty) may come with null cache pointers.
   if (num_pages > 0 && (!k_cache || !v_cache)) return RLDA_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out)) return RLDA_ERR_INVALID_ARG;
   if (((uintptr_t)block_table & 3u) || ((uintptr_t)seq_lens & 3u)) return RLDA_ERR_INVALID_ARG;
+  if (grouped && (!prefix_pages || ((uintptr_t)prefix_pages & 3u))) return RLDA_ERR_INVALID_ARG;
   const bool fp8 = h->kind == rlda::KvKind::FP8;
   if (fp8 && num_pages > 0 && (!k_scale || !v_scale || ((uintptr_t)k_scale & 3u) || ((uintptr_t)v_scale & 3u)))
     return RLDA_ERR_INVALID_ARG;
   const WsLayout wl = layout_of(h);
   if (!workspace || ((uintptr_t)workspace % kAlign)) return RLDA_ERR_WORKSPACE;
-  if (workspace_bytes < wl.total) return RLDA_ERR_WORKSPACE;
+  if (workspace_bytes < (grouped ? wl.grouped_total : wl.total)) return RLDA_ERR_WORKSPACE;
 
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return RLDA_ERR_HIP;
@@ -212,7 +228,31 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, const
   p.scale_log2 = h->scale * 1.4426950408889634f;
   p.out_bf16 = c.out_dtype == RLDA_BF16;
   memcpy(p.q_head, h->q_head, sizeof p.q_head);
-  if (rlda::launch_decode(h->kind, c.head_dim, h->group, p, stream, ev_begin, ev_end) != hipSuccess)
+  if (!grouped) {
+    if (rlda::launch_decode(h->kind, c.head_dim, h->group, p, stream, ev_begin, ev_end) != hipSuccess)
+      return RLDA_ERR_HIP;
+    return RLDA_OK;
+  }
+  p.prefix_pages = prefix_pages;
+  p.gprefix = (int32_t*)(ws + wl.gprefix);
+  p.pfx_ml = (float*)(ws + wl.pfx_ml);
+  p.pfx_acc = (float*)(ws + wl.pfx_acc);
+  p.group_size = group_size;
+  // Prompt-pass jobs: up to 64 query rows (4 MFMA tiles) of G heads per member.
+  p.pfx_mblock = group_size < 64 / h->group ? group_size : 64 / h->group;
+  p.pfx_nblocks = (group_size + p.pfx_mblock - 1) / p.pfx_mblock;
+  const int ngroups = (batch + group_size - 1) / group_size;
+  const int64_t jobs = (int64_t)ngroups * c.num_kv_heads * p.pfx_nblocks;
+  if (jobs * rlda::kMaxRanges > INT32_MAX) return RLDA_ERR_UNSUPPORTED;
+  // Split each job over several workgroups until the prompt pass fills the CUs,
+  // within the partial-slot capacity the workspace has (64-row slots).
+  const int64_t slots = 2 * (int64_t)h->ws_ranges * h->group / 64;
+  int64_t split = jobs >= ranges ? 1 : ranges / jobs;
+  if (split > 8) split = 8;
+  if (split * jobs > slots) split = slots / jobs;
+  p.pfx_splits = split < 1 ? 1 : (int)split;
+  p.pfx_slots = (int)(slots < INT32_MAX ? slots : INT32_MAX);
+  if (rlda::launch_grouped(h->kind, c.head_dim, h->group, p, ngroups, stream, ev_begin, ev_end) != hipSuccess)
     return RLDA_ERR_HIP;
   return RLDA_OK;
 }
@@ -225,8 +265,8 @@ rlda_status rl_decode_attn_run(rl_decode_attn_t h, int32_t batch, int32_t num_pa
                                const void* k_cache, const void* v_cache, const float* k_scale,
                                const float* v_scale, const int32_t* block_table, const int32_t* seq_lens,
                                void* out, void* workspace, size_t workspace_bytes, void* stream) {
-  return run_impl(h, batch, num_pages, q, k_cache, v_cache, k_scale, v_scale, block_table, seq_lens, out,
-                  workspace, workspace_bytes, stream, nullptr, nullptr);
+  return run_impl(h, batch, num_pages, 0, nullptr, q, k_cache, v_cache, k_scale, v_scale, block_table, seq_lens,
+                  out, workspace, workspace_bytes, stream, nullptr, nullptr);
 }
 
 rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t h, int32_t batch, int32_t num_pages, const void* q,
@@ -236,8 +276,19 @@ rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t h, int32_t batch, int32
                                         size_t workspace_bytes, void* stream, void* event_begin,
                                         void* event_end) {
   if (!event_begin || !event_end) return RLDA_ERR_INVALID_ARG;
-  return run_impl(h, batch, num_pages, q, k_cache, v_cache, k_scale, v_scale, block_table, seq_lens, out,
-                  workspace, workspace_bytes, stream, event_begin, event_end);
+  return run_impl(h, batch, num_pages, 0, nullptr, q, k_cache, v_cache, k_scale, v_scale, block_table, seq_lens,
+                  out, workspace, workspace_bytes, stream, event_begin, event_end);
+}
+
+rlda_status rl_decode_attn_run_grouped(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32_t group_size,
+                                       const int32_t* prefix_pages, const void* q, const void* k_cache,
+                                       const void* v_cache, const float* k_scale, const float* v_scale,
+                                       const int32_t* block_table, const int32_t* seq_lens, void* out,
+                                       void* workspace, size_t workspace_bytes, void* stream, void* event_begin,
+                                       void* event_end) {
+  if (group_size < 1 || (!event_begin) != (!event_end)) return RLDA_ERR_INVALID_ARG;
+  return run_impl(h, batch, num_pages, group_size, prefix_pages, q, k_cache, v_cache, k_scale, v_scale,
+                  block_table, seq_lens, out, workspace, workspace_bytes, stream, event_begin, event_end);
 }
 
 rlda_status rl_decode_attn_read_flags(rl_decode_attn_t h, const void* workspace, void* stream, uint32_t* flags) {

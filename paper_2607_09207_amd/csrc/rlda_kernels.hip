@@ -295,12 +295,67 @@ struct Mfma {
       qo.v[s] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, row + 16 * chunk_of(qg, s), 0, 0));
   }
 
+  // Q operand of the prompt pass: row r of the tile (lane group i = r) is query
+  // head (row % G) of sequence b_first + row / G with row = row0 + r; rows at or
+  // past `rows` read zeros.
+  __device__ __forceinline__ static void load_q_rows(QOp& qo, const Params& p, int g, int b_first, int rows, int row0,
+                                                     int lane) {
+    const int i = lane & 15, qg = lane >> 4;
+    const int G = p.group, row = row0 + i;
+    const __amdgpu_buffer_rsrc_t r = make_rsrc_uni(p.q, (uint32_t)p.batch * (uint32_t)p.num_q_heads * D * 2u);
+    int off = kPastRange;
+    if (row < rows) {
+      const int b = b_first + row / G, h = s_qhead[g * G + row % G];
+      off = (b * p.num_q_heads + h) * D * 2;
+    }
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      qo.v[s] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, off + 16 * chunk_of(qg, s), 0, 0));
+  }
+
   // Start accumulating a new (sequence, KV head) with its Q operand.
   __device__ __forceinline__ void begin(const QOp& qo, const Params&, int, int, int) {
 #pragma unroll
     for (int t = 0; t < DT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     m = neg_inf();
     l = 0.f;
+    q = qo;
+  }
+
+  // State of a grouped run's prompt pass for one (sequence, KV head), loaded with
+  // the segment's first page: lane 16q + i gets O[head i][D/16*(4q+r) + t] for
+  // r < 4, t < D/16, and (m, l) of head i.
+  struct PInit {
+    u32x4 a[DT];
+    u32x2 ml;
+  };
+  __device__ __forceinline__ static void load_prompt(PInit& pi, const Params& p, int b, int g, int lane, bool load) {
+    if (!load) return;
+    const int i = lane & 15, qg = lane >> 4;
+    const int G = p.group, Hq = p.num_q_heads;
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc_uni(p.pfx_acc + (int64_t)b * Hq * D, (uint32_t)(Hq * D * 4));
+    const __amdgpu_buffer_rsrc_t rm = make_rsrc_uni(p.pfx_ml + (int64_t)b * Hq * 2, (uint32_t)(Hq * 8));
+    const int h = (i < G) ? s_qhead[g * G + i] : 0;
+    const int orow = (i < G) ? h * D * 4 : kPastRange, mrow = (i < G) ? h * 8 : kPastRange;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int c = 0; c < DT; c += 4)
+        pi.a[r * (DT / 4) + c / 4] = __builtin_amdgcn_raw_buffer_load_b128(ra, orow + (DT * (4 * qg + r) + c) * 4, 0, 0);
+    pi.ml = __builtin_amdgcn_raw_buffer_load_b64(rm, mrow, 0, 0);
+  }
+
+  // Start a segment from the prompt pass's state (the first piece of a grouped
+  // sequence's remaining pages).  The lane-group partial sums of l add up to the
+  // prompt's sum: lane group 0 carries it.
+  __device__ __forceinline__ void begin_prompt(const QOp& qo, const PInit& pi, int G, int lane) {
+    const int i = lane & 15, qg = lane >> 4;
+#pragma unroll
+    for (int t = 0; t < DT; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[t][r] = __uint_as_float(pi.a[r * (DT / 4) + t / 4][t % 4]);
+    m = (i < G) ? __uint_as_float(pi.ml[0]) : neg_inf();
+    l = (i < G && qg == 0) ? __uint_as_float(pi.ml[1]) : 0.f;
     q = qo;
   }
 
@@ -443,6 +498,7 @@ struct Valu {
   };
   struct QOp {};
   static constexpr bool kQRing = false;   // q is loaded when a segment begins
+  struct PInit {};                        // grouped runs are not supported with fp32 caches
 
   float acc[GM][CW];
   float qv[GM][CW];
@@ -454,6 +510,7 @@ struct Valu {
   }
 
   __device__ __forceinline__ static void load_q(QOp&, const Params&, int, int, int, bool) {}
+  __device__ __forceinline__ static void load_prompt(PInit&, const Params&, int, int, int, bool) {}
 
   __device__ __forceinline__ void begin(const QOp&, const Params& p, int b, int g, int lane) {
     const int c = lane & 3;
@@ -560,7 +617,8 @@ constexpr int kInfoLast = 1 << 6;       // last page of its (sequence, KV head)
 constexpr int kInfoStart = 1 << 7;      // first position of this wave's quarter
 constexpr int kInfoEnd = 1 << 8;        // last position of this wave's quarter
 constexpr int kInfoHeadShift = 9;       // KV head g: 8 bits
-constexpr int kInfoSeqShift = 17;       // sequence b: up to 14 bits
+constexpr int kInfoSeqShift = 17;       // sequence b: 13 bits (b < 8192)
+constexpr int kInfoPrompt = 1 << 30;    // grouped run: the sequence's prompt pass state seeds its first page
 
 // The page id is returned as read; it is checked where it is used, so that
 // nothing waits for these loads until the chunk is consumed.
@@ -571,7 +629,7 @@ struct StreamChunk {
 
 // Positions fit in 32 bits: the host rejects max_batch * max_pages * Hkv >= 2^31.
 __device__ __forceinline__ StreamChunk fetch_chunk(const Params& p, const int32_t* s_pre, const uint8_t* s_tail,
-                                                   int base, int w0, int w1, int lane) {
+                                                   const int32_t* s_ppre, int base, int w0, int w1, int lane) {
   StreamChunk c = {-1, 0};
   const int pos = base + lane;
   if (pos < w1) {
@@ -586,9 +644,11 @@ __device__ __forceinline__ StreamChunk fetch_chunk(const Params& p, const int32_
     const int off = pos - Hkv * pre;
     const int g = (int)((uint32_t)off / (uint32_t)nb), j = off - g * nb;
     const int tok = (j == nb - 1) ? s_tail[b] : kPage;
-    c.pid = p.block_table[(int64_t)b * p.max_pages + j];
+    const int pp = s_ppre[b];   // prompt pages handled by the prompt pass (grouped runs)
+    c.pid = p.block_table[(int64_t)b * p.max_pages + pp + j];
     c.info = tok | (j == 0 ? kInfoFirst : 0) | (j == nb - 1 ? kInfoLast : 0) | (pos == w0 ? kInfoStart : 0) |
-             (pos == w1 - 1 ? kInfoEnd : 0) | (g << kInfoHeadShift) | (b << kInfoSeqShift);
+             (pos == w1 - 1 ? kInfoEnd : 0) | (g << kInfoHeadShift) | (b << kInfoSeqShift) |
+             (pp > 0 ? kInfoPrompt : 0);
   }
   return c;
 }
@@ -602,6 +662,7 @@ void decode_attention_kernel(const Params p) {
   constexpr int DPT = D / 16;   // output elements per thread in the workgroup merge
   __shared__ int32_t s_pre[kMaxBatch + 1];
   __shared__ uint8_t s_tail[kMaxBatch];   // valid tokens of each sequence's last page
+  __shared__ int32_t s_ppre[kMaxBatch];   // grouped runs: leading pages covered by the prompt pass
   // Cut pieces: slot 2w holds wave w's piece that began before its quarter of the
   // share, slot 2w+1 its piece that continues past it.
   __shared__ __align__(16) float s_acc[2 * kWaves][16][D + 4];
@@ -632,9 +693,14 @@ void decode_attention_kernel(const Params p) {
       int L = p.seq_lens[b];
       if (L < 0 || L > cap) bad = 1;
       L = min(max(L, 0), cap);
-      const int n = (L + kPage - 1) / kPage;
+      const int nfull = (L + kPage - 1) / kPage;
+      // Grouped runs: the prompt pass covered the first pp pages (its clamp keeps
+      // pp <= floor(L / 16)); this kernel streams the rest.
+      const int pp = p.group_size > 0 ? min(max(p.gprefix[b / p.group_size], 0), L / kPage) : 0;
+      const int n = nfull - pp;
+      s_ppre[b] = pp;
       s_pre[b + 1] = n;
-      s_tail[b] = (uint8_t)(L - (n - 1) * kPage);   // 1..16 when n > 0
+      s_tail[b] = (uint8_t)(L - (nfull - 1) * kPage);   // 1..16 when nfull > 0
       sum += n;
     }
     if (bad && u == 0) atomicOr(p.flags, kFlagBadLen);
@@ -659,15 +725,23 @@ void decode_attention_kernel(const Params p) {
   }
   const int64_t T = uni64((int64_t)s_pre[batch] * Hkv);
 
-  // 2. Sequences with no tokens get zero rows.
+  // 2. Sequences with no pages left to stream: zero rows, or (grouped runs) the
+  //    normalised prompt-pass result when the prompt is the whole sequence.
   for (int b = u; b < batch; b += W) {
     if (s_pre[b + 1] != s_pre[b]) continue;
     const int n = p.num_q_heads * D;
+    const bool prompt = s_ppre[b] > 0;
     for (int e = tid; e < n; e += kThreads) {
+      float v = 0.f;
+      if (prompt) {
+        const int64_t row = (int64_t)b * p.num_q_heads + e / D;
+        const float ls = p.pfx_ml[row * 2 + 1];
+        v = ls > 0.f ? p.pfx_acc[(int64_t)b * n + e] / ls : 0.f;
+      }
       if (p.out_bf16)
-        ((uint16_t*)p.out)[(int64_t)b * n + e] = 0;
+        ((uint16_t*)p.out)[(int64_t)b * n + e] = __builtin_bit_cast(uint16_t, (__bf16)v);
       else
-        ((float*)p.out)[(int64_t)b * n + e] = 0.f;
+        ((float*)p.out)[(int64_t)b * n + e] = v;
     }
   }
 
@@ -686,18 +760,19 @@ void decode_attention_kernel(const Params p) {
     Pol st;
     st.setup(p, lane, p.stride_slot);
     typename Pol::QOp qring[kDepth];
+    typename Pol::PInit pring[kDepth];
     bool began = false;   // the segment being accumulated began inside this quarter
-    StreamChunk nxt = fetch_chunk(p, s_pre, s_tail, w0, w0, w1, lane);
+    StreamChunk nxt = fetch_chunk(p, s_pre, s_tail, s_ppre, w0, w0, w1, lane);
     for (int base = w0; base < w1; base += kChunk) {
       const StreamChunk cur = nxt;
       const int cn = min(kChunk, w1 - base);
-      if (base + kChunk < w1) nxt = fetch_chunk(p, s_pre, s_tail, base + kChunk, w0, w1, lane);
+      if (base + kChunk < w1) nxt = fetch_chunk(p, s_pre, s_tail, s_ppre, base + kChunk, w0, w1, lane);
       typename Pol::Frag fr[kDepth];
       int sinfo[kDepth];
       float skm[kDepth], svm[kDepth];
       // Issue the loads of position base + k into pipeline slot `sl`.
       auto issue = [&](typename Pol::Frag& f, int& info_out, float& km_out, float& vm_out,
-                       typename Pol::QOp& q_out, int k) {
+                       typename Pol::QOp& q_out, typename Pol::PInit& pi_out, int k) {
         int pk = -1, info = 0;
         float ks = 1.f, vs = 1.f;
         if (k < cn) {
@@ -710,7 +785,7 @@ void decode_attention_kernel(const Params p) {
           }
         }
         const int tok = info & kInfoTok;
-        const int g = (info >> kInfoHeadShift) & 255, b = info >> kInfoSeqShift;
+        const int g = (info >> kInfoHeadShift) & 255, b = (info >> kInfoSeqShift) & 8191;
         if constexpr (Pol::kFp8) {
           // Scales of (page, KV head); no records (reads of zero) for an absent page.
           const int64_t si = (pk >= 0) ? (int64_t)pk * Hkv + g : 0;
@@ -721,18 +796,28 @@ void decode_attention_kernel(const Params p) {
         const int64_t po = (pk >= 0) ? (int64_t)pk * p.stride_page + (int64_t)g * p.stride_head : 0;
         const uint32_t nrec = tok > 0 ? (uint32_t)((tok - 1) * p.stride_slot + D * Pol::kEB) : 0u;
         st.issue(f, make_rsrc_uni((const char*)p.k + po, nrec), make_rsrc_uni((const char*)p.v + po, nrec));
-        if constexpr (Pol::kQRing) Pol::load_q(q_out, p, b, g, lane, (info & (kInfoFirst | kInfoStart)) != 0);
+        if constexpr (Pol::kQRing) {
+          Pol::load_q(q_out, p, b, g, lane, (info & (kInfoFirst | kInfoStart)) != 0);
+          Pol::load_prompt(pi_out, p, b, g, lane, (info & kInfoFirst) && (info & kInfoPrompt));
+        }
         info_out = info;   // the scales are used as loaded, in compute
         km_out = ks;
         vm_out = vs;
       };
       // Consume pipeline slot `sl` (position base + k).
       auto compute = [&](const typename Pol::Frag& f, int info, float km, float vm, const typename Pol::QOp& q,
-                         int k) {
+                         const typename Pol::PInit& pi, int k) {
         if (k >= cn) return;
-        const int g = (info >> kInfoHeadShift) & 255, b = info >> kInfoSeqShift;
+        const int g = (info >> kInfoHeadShift) & 255, b = (info >> kInfoSeqShift) & 8191;
         if (info & (kInfoFirst | kInfoStart)) {
-          st.begin(q, p, b, g, lane);
+          bool seeded = false;
+          if constexpr (Pol::kQRing) {
+            if ((info & kInfoFirst) && (info & kInfoPrompt)) {
+              st.begin_prompt(q, pi, G, lane);
+              seeded = true;
+            }
+          }
+          if (!seeded) st.begin(q, p, b, g, lane);
           began = (info & kInfoFirst) != 0;
         }
         st.compute(f, lane, info & kInfoTok, p.scale_log2 * km, vm);
@@ -749,15 +834,15 @@ void decode_attention_kernel(const Params p) {
       };
 #pragma unroll
       for (int k = 0; k < kDepth - 1; ++k)
-        if (k < cn) issue(fr[k], sinfo[k], skm[k], svm[k], qring[k], k);
+        if (k < cn) issue(fr[k], sinfo[k], skm[k], svm[k], qring[k], pring[k], k);
       int i = 0;
       // Steady state: every position issued lies inside the chunk.
       for (; i + 2 * kDepth - 2 < cn; i += kDepth) {
 #pragma unroll
         for (int k = 0; k < kDepth; ++k) {
           const int si = (k + kDepth - 1) % kDepth;
-          issue(fr[si], sinfo[si], skm[si], svm[si], qring[si], i + k + kDepth - 1);
-          compute(fr[k], sinfo[k], skm[k], svm[k], qring[k], i + k);
+          issue(fr[si], sinfo[si], skm[si], svm[si], qring[si], pring[si], i + k + kDepth - 1);
+          compute(fr[k], sinfo[k], skm[k], svm[k], qring[k], pring[k], i + k);
         }
       }
       // Drain: no loads are issued past the chunk, so none is left in flight.
@@ -765,8 +850,9 @@ void decode_attention_kernel(const Params p) {
 #pragma unroll
         for (int k = 0; k < kDepth; ++k) {
           const int si = (k + kDepth - 1) % kDepth;
-          if (i + k + kDepth - 1 < cn) issue(fr[si], sinfo[si], skm[si], svm[si], qring[si], i + k + kDepth - 1);
-          compute(fr[k], sinfo[k], skm[k], svm[k], qring[k], i + k);
+          if (i + k + kDepth - 1 < cn)
+            issue(fr[si], sinfo[si], skm[si], svm[si], qring[si], pring[si], i + k + kDepth - 1);
+          compute(fr[k], sinfo[k], skm[k], svm[k], qring[k], pring[k], i + k);
         }
       }
     }
@@ -860,6 +946,189 @@ void decode_attention_kernel(const Params p) {
   }
 }
 
+// ---------------------------------------------------------------- prompt pass (grouped runs)
+// One workgroup per job (group i, KV head g, member block): the job's query rows
+// are the G heads of each of up to 64/G members (row = (member - first) * G +
+// head index), packed into up to 4 MFMA tiles of 16 rows.  The 4 waves split the
+// group's prompt pages; each page is loaded once and multiplied against every
+// tile, so the group reads its prompt once per KV head instead of once per
+// response.  The 4 waves' states are merged through LDS and each row's
+// unnormalised (m, l, O) is stored for the attention kernel, which continues
+// every member's softmax from it.  The job of block 0 of KV head 0 also stores
+// the group's clamped prompt length.
+constexpr int kPromptTiles = 4;
+
+template <int D, bool FP8>
+__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(1, 1)))
+void prompt_kernel(const Params p) {
+  using Pol = Mfma<D, FP8>;
+  constexpr int R = kPromptTiles, kRows = 16 * R, kDepth = Pol::kDepth;
+  __shared__ __align__(16) float s_acc[kWaves][kRows][D + 4];
+  __shared__ __align__(16) float s_ml[kWaves][kRows][2];
+  __shared__ int32_t s_min;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
+  const int Hkv = p.num_kv_heads, G = p.group, Hq = p.num_q_heads, n = p.group_size;
+  const int cap = p.max_pages * kPage;
+  const int job = blockIdx.x / p.pfx_splits, split = blockIdx.x - job * p.pfx_splits;
+  const int mb = job % p.pfx_nblocks, ig = job / p.pfx_nblocks;
+  const int g = ig % Hkv, gi = ig / Hkv;
+  const int b0 = gi * n, b1 = min(b0 + n, p.batch);                        // members of group gi
+  const int m0 = b0 + mb * p.pfx_mblock, m1 = min(m0 + p.pfx_mblock, b1);  // members of this job
+
+  for (int e = tid; e < Hq; e += kThreads) s_qhead[e] = p.q_head[e];
+  if (tid == 0) s_min = 0x7fffffff;
+  __syncthreads();
+  // Shared prompt: the requested pages, clamped to the full pages of the shortest member.
+  {
+    int mn = 0x7fffffff;
+    for (int b = b0 + tid; b < b1; b += kThreads) mn = min(mn, min(max(p.seq_lens[b], 0), cap) / kPage);
+    if (mn != 0x7fffffff) atomicMin(&s_min, mn);
+  }
+  __syncthreads();
+  const int want = p.prefix_pages[gi];
+  const int P = uni(max(0, min(want, s_min)));
+  if (tid == 0 && g == 0 && mb == 0 && split == 0) {
+    p.gprefix[gi] = P;
+    if (want != P) atomicOr(p.flags, kFlagPrefixClamped);
+  }
+  const int rows = (m1 - m0) * G;
+  // Workgroups per job: at least 32 pages each (8 per wave), at most the launched
+  // p.pfx_splits; the others have nothing to do.  A split costs a device-scope
+  // handoff, which only pays off for long prompts.
+  const int S = uni(min(p.pfx_splits, max(1, (P + 31) / 32)));
+  if (P == 0 || rows <= 0 || split >= S) return;
+  const int nt = uni((rows + 15) / 16);   // tiles in use
+
+  Pol t[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    t[r].setup(p, lane, p.stride_slot);
+    typename Pol::QOp qo;
+    Pol::load_q_rows(qo, p, g, m0, rows, 16 * r, lane);
+    t[r].begin(qo, p, 0, 0, lane);
+  }
+
+  // This wave's prompt pages [j0, j1) (the job's pages cut into S * 4 ranges), read
+  // from the group's first member's row.
+  const int ws = split * kWaves + wave;
+  const int j0 = ws * P / (S * kWaves), j1 = (ws + 1) * P / (S * kWaves);
+  const int32_t* bt = p.block_table + (int64_t)b0 * p.max_pages;
+  const int rec = (kPage - 1) * p.stride_slot + D * Pol::kEB;   // a full page
+  for (int cb = j0; cb < j1; cb += kChunk) {
+    const int cn = min(kChunk, j1 - cb);
+    int pid = bt[cb + min(lane, cn - 1)];
+    typename Pol::Frag fr[kDepth];
+    float skm[kDepth], svm[kDepth];
+    int sval[kDepth];
+    // Every step issues the same loads (past the range with descriptors of no
+    // records, which read nothing), so the loads stay in flight across steps.
+    auto issue = [&](typename Pol::Frag& f, int& val, float& ks, float& vs, int k) {
+      int pk = -1;
+      if (k < cn) {
+        pk = __builtin_amdgcn_readlane(pid, k);
+        if ((unsigned)pk >= (unsigned)p.num_pages) {   // not a page of the pool: contributes nothing
+          if (lane == 0) atomicOr(p.flags, kFlagBadPage);
+          pk = -1;
+        }
+      }
+      val = pk >= 0 ? kPage : 0;
+      const int64_t po = (pk >= 0) ? (int64_t)pk * p.stride_page + (int64_t)g * p.stride_head : 0;
+      const uint32_t nrec = pk >= 0 ? (uint32_t)rec : 0u;
+      ks = 1.f;
+      vs = 1.f;
+      if constexpr (FP8) {
+        const int64_t si = (pk >= 0) ? (int64_t)pk * Hkv + g : 0;
+        const uint32_t sb = (pk >= 0) ? 4u : 0u;
+        ks = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(make_rsrc_uni(p.k_scale + si, sb), 0, 0, 0));
+        vs = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(make_rsrc_uni(p.v_scale + si, sb), 0, 0, 0));
+      }
+      t[0].issue(f, make_rsrc_uni((const char*)p.k + po, nrec), make_rsrc_uni((const char*)p.v + po, nrec));
+    };
+    auto compute = [&](const typename Pol::Frag& f, int val, float ks, float vs) {
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+        if (r < nt) t[r].compute(f, lane, val, p.scale_log2 * ks, vs);
+    };
+#pragma unroll
+    for (int k = 0; k < kDepth - 1; ++k) issue(fr[k], sval[k], skm[k], svm[k], k);
+    for (int i = 0; i < cn; i += kDepth) {
+#pragma unroll
+      for (int k = 0; k < kDepth; ++k) {
+        const int si = (k + kDepth - 1) % kDepth;
+        issue(fr[si], sval[si], skm[si], svm[si], i + k + kDepth - 1);
+        if (i + k < cn) compute(fr[k], sval[k], skm[k], svm[k]);
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) t[r].to_lds(s_acc[wave] + 16 * r, s_ml[wave] + 16 * r, lane);
+  __syncthreads();
+
+  // Merge the 4 waves' states: thread (row, quarter of d).
+  constexpr int DQ = D / 4;
+  const int row = tid >> 2, d0 = (tid & 3) * DQ;
+  float M = neg_inf(), Ls = 0.f, o[DQ];
+#pragma unroll
+  for (int e = 0; e < DQ; ++e) o[e] = 0.f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    float v[DQ];
+#pragma unroll
+    for (int c = 0; c < DQ; c += 4) *(f32x4*)&v[c] = *(const f32x4*)&s_acc[w][row][d0 + c];
+    lse_merge<DQ>(M, Ls, o, s_ml[w][row][0], s_ml[w][row][1], v);
+  }
+  if (S > 1) {
+    // The job is split over S workgroups: publish this one's state in slot
+    // job * S + split (device scope, rows of 64), count it, and let the workgroup
+    // that completes the count merge the S states in split order.
+    const __amdgpu_buffer_rsrc_t ra = make_rsrc_uni(p.part_acc, (uint32_t)p.pfx_slots * kRows * D * 4u);
+    const __amdgpu_buffer_rsrc_t rm = make_rsrc_uni(p.part_ml, (uint32_t)p.pfx_slots * kRows * 8u);
+    const int slot_row = (job * p.pfx_splits + split) * kRows + row;
+#pragma unroll
+    for (int c = 0; c < DQ; c += 4)
+      __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(o[c]), __float_as_uint(o[c + 1]),
+                                                   __float_as_uint(o[c + 2]), __float_as_uint(o[c + 3])},
+                                             ra, (slot_row * D + d0 + c) * 4, 0, kDeviceScope);
+    if ((tid & 3) == 0)
+      __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(M), __float_as_uint(Ls)}, rm, slot_row * 8, 0,
+                                            kDeviceScope);
+    __builtin_amdgcn_s_waitcnt(0);   // this wave's device-scope stores have completed
+    __syncthreads();                 // ... and every other wave's
+    if (tid == 0) s_min = (atomicAdd(p.counters + job, 1u) + 1u == (uint32_t)S);
+    __syncthreads();
+    if (!s_min) return;
+    if (tid == 0) atomicExch(p.counters + job, 0u);
+    M = neg_inf();
+    Ls = 0.f;
+#pragma unroll
+    for (int e = 0; e < DQ; ++e) o[e] = 0.f;
+    constexpr int kBatch = 4;
+    for (int k0 = 0; k0 < S; k0 += kBatch) {
+      u32x2 ml[kBatch];
+      float v[kBatch][DQ];
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) {
+        const int sr = (job * p.pfx_splits + min(k0 + i, S - 1)) * kRows + row;   // past the last split: re-read, unused
+        ml[i] = __builtin_amdgcn_raw_buffer_load_b64(rm, sr * 8, 0, kDeviceScope);
+#pragma unroll
+        for (int c = 0; c < DQ; c += 4)
+          *(u32x4*)&v[i][c] = __builtin_amdgcn_raw_buffer_load_b128(ra, (sr * D + d0 + c) * 4, 0, kDeviceScope);
+      }
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i)
+        if (k0 + i < S) lse_merge<DQ>(M, Ls, o, __uint_as_float(ml[i][0]), __uint_as_float(ml[i][1]), v[i]);
+    }
+  }
+  if (row >= rows) return;
+  const int b = m0 + row / G, h = s_qhead[g * G + row % G];
+  const int64_t orow = (int64_t)b * Hq + h;
+  float* dst = p.pfx_acc + orow * D + d0;
+#pragma unroll
+  for (int c = 0; c < DQ; c += 4) *(f32x4*)(dst + c) = f32x4{o[c], o[c + 1], o[c + 2], o[c + 3]};
+  if ((tid & 3) == 0) *(f32x2*)(p.pfx_ml + orow * 2) = f32x2{M, Ls};
+}
+
 template <class Pol>
 int launch(const Params& p, void* stream, void* ev_begin, void* ev_end) {
   hipStream_t st = (hipStream_t)stream;
@@ -869,6 +1138,17 @@ int launch(const Params& p, void* stream, void* ev_begin, void* ev_end) {
   if (e != hipSuccess) return (int)e;
   if (ev_end && hipEventRecord((hipEvent_t)ev_end, st) != hipSuccess) return -1;
   return 0;
+}
+
+template <int D, bool FP8>
+int launch_prompt_then_decode(const Params& p, int ngroups, void* stream, void* ev_begin, void* ev_end) {
+  hipStream_t st = (hipStream_t)stream;
+  if (ev_begin && hipEventRecord((hipEvent_t)ev_begin, st) != hipSuccess) return -1;
+  const int jobs = ngroups * p.num_kv_heads * p.pfx_nblocks;
+  hipLaunchKernelGGL((prompt_kernel<D, FP8>), dim3(jobs * p.pfx_splits), dim3(kThreads), 0, st, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return (int)e;
+  return launch<Mfma<D, FP8>>(p, stream, nullptr, ev_end);
 }
 
 }  // namespace
@@ -890,6 +1170,21 @@ int launch(const Params& p, void* stream, void* ev_begin, void* ev_end) {
 int launch_decode(KvKind kind, int head_dim, int group, const Params& p, void* stream, void* ev_begin,
                   void* ev_end) {
   RLDA_DISPATCH(launch, p, stream, ev_begin, ev_end)
+}
+
+int launch_grouped(KvKind kind, int head_dim, int, const Params& p, int ngroups, void* stream, void* ev_begin,
+                   void* ev_end) {
+  switch (kind) {
+    case KvKind::BF16:
+      return head_dim == 128 ? launch_prompt_then_decode<128, false>(p, ngroups, stream, ev_begin, ev_end)
+                             : launch_prompt_then_decode<64, false>(p, ngroups, stream, ev_begin, ev_end);
+    case KvKind::FP8:
+      return head_dim == 128 ? launch_prompt_then_decode<128, true>(p, ngroups, stream, ev_begin, ev_end)
+                             : launch_prompt_then_decode<64, true>(p, ngroups, stream, ev_begin, ev_end);
+    case KvKind::F32:
+      break;
+  }
+  return -1;
 }
 
 

@@ -15,6 +15,7 @@ constexpr int kMaxGroup = 16;      // query heads per KV head packed in one MFMA
 // Bits of the device-side contract flag word.
 constexpr uint32_t kFlagBadPage = 1u;
 constexpr uint32_t kFlagBadLen = 2u;
+constexpr uint32_t kFlagPrefixClamped = 4u;
 
 struct Params {
   const void* q;               // [batch][Hq][D]
@@ -41,6 +42,16 @@ struct Params {
   int32_t nranges;             // workgroups = equal shares of the flattened work
   float scale_log2;            // softmax scale * log2(e)
   int32_t out_bf16;            // 0: fp32 output, 1: bf16 output
+  // Shared-prompt (grouped) runs; all null / 0 otherwise.
+  const int32_t* prefix_pages; // [ngroups] requested prompt pages per group (device)
+  int32_t* gprefix;            // [ngroups] prompt pages after the clamp (written by the prompt pass)
+  float* pfx_acc;              // [batch][Hq][D] prompt-pass unnormalised outputs
+  float* pfx_ml;               // [batch][Hq][2] prompt-pass (max in log2 units, sum)
+  int32_t group_size;          // sequences per group; 0: not grouped
+  int32_t pfx_mblock;          // members per prompt-pass job (rows = members * G <= 64)
+  int32_t pfx_nblocks;         // jobs per (group, KV head)
+  int32_t pfx_splits;          // workgroups per job (their states meet in the partial slots)
+  int32_t pfx_slots;           // capacity of part_acc / part_ml in 64-row prompt-pass slots
   int16_t q_head[kMaxQHeads];  // q_head[g * G + i] = i-th query head of KV head g
 };
 
@@ -50,5 +61,9 @@ enum class KvKind { F32, BF16, FP8 };
 // The kernel is bracketed by ev_begin / ev_end when they are non-null.
 int launch_decode(KvKind kind, int head_dim, int group, const Params& p, void* stream, void* ev_begin,
                   void* ev_end);
+// Prompt pass of a grouped run (one workgroup per (group, KV head, member block)),
+// followed by the attention kernel.
+int launch_grouped(KvKind kind, int head_dim, int group, const Params& p, int ngroups, void* stream,
+                   void* ev_begin, void* ev_end);
 
 }  // namespace rlda

@@ -275,12 +275,15 @@ def gqa_longtail_bf16(seed=1001):
     return _scattered("gqa_longtail_bf16", seed, rng, lens, 28, 4, 128, "bf16", "bf16", 1024)
 
 
-def grpo_shared_prefix_bf16(seed=1002):
+def grpo_shared_prefix_bf16(seed=1002, prompt_len=512):
     """32 prompts x 8 responses, 12 query / 2 KV heads, d=128, bf16.  Each prompt has
     512 tokens (32 full pages) shared through the block table by its 8 responses;
-    response tails lognormal (median 1024, sigma 1.2) clipped to [1, 24576]."""
+    response tails lognormal (median 1024, sigma 1.2) clipped to [1, 24576].
+    `prompt_len` (a multiple of 16) varies the prompt length for sweeps; the
+    workload keeps its name only at the default."""
+    assert prompt_len > 0 and prompt_len % PAGE_SIZE == 0
     rng = np.random.default_rng(seed)
-    prompts, group, prompt_len = 32, 8, 512
+    prompts, group = 32, 8
     tails = _lognormal_lengths(rng, prompts * group, 1024, 1.2, 1, 24576)
     lens = prompt_len + tails
     prompt_pages = prompt_len // PAGE_SIZE
@@ -296,7 +299,8 @@ def grpo_shared_prefix_bf16(seed=1002):
         cur += tail_pages[b]
         rows.append(np.concatenate([shared, own]))
     bt = _table(rows, prompts * group, max_pages)
-    return build_workload("grpo_shared_prefix_bf16", seed, lens, bt, n_pages, 12, 2, 128, "bf16", "bf16",
+    name = "grpo_shared_prefix_bf16" if prompt_len == 512 else f"grpo_shared_prefix_bf16_prompt{prompt_len}"
+    return build_workload(name, seed, lens, bt, n_pages, 12, 2, 128, "bf16", "bf16",
                           max_pages, shared_prefix_tokens=prompt_len, group_size=group)
 
 

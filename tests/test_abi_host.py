@@ -151,3 +151,35 @@ def test_workspace_grows_with_forced_ranges_and_heads(lib):
         sizes.append(n.value)
         lib.rl_decode_attn_destroy(h)
     assert sizes[0] < sizes[1] < sizes[2]
+
+
+def test_grouped_run_rejects_bad_arguments_before_launch(lib):
+    st, h = create(lib, cfg(num_q_heads=12, num_kv_heads=2, max_batch=256, max_pages_per_seq=1568))
+    assert st == 0
+    n, ng = ctypes.c_size_t(), ctypes.c_size_t()
+    lib.rl_decode_attn_workspace_size(h, ctypes.byref(n))
+    assert lib.rl_decode_attn_grouped_workspace_size(h, ctypes.byref(ng)) == 0
+    # the prompt pass adds per-row (m, l, O) and one clamped length per group
+    assert ng.value >= n.value + 256 * (12 * (128 + 2) + 1) * 4 and ng.value % 256 == 0
+    f = 0x10000
+
+    def run(batch=8, gs=4, pp=f, wsb=None, e0=None, e1=None, handle=h):
+        return lib.rl_decode_attn_run_grouped(handle, batch, 10, gs, pp, f, f, f, None, None, f, f, f, f * 16,
+                                              ng.value if wsb is None else wsb, None, e0, e1)
+
+    assert run(gs=0) == -1                # group size must be >= 1
+    assert run(gs=-3) == -1
+    assert run(pp=None) == -1             # prefix_pages required
+    assert run(pp=f + 2) == -1            # misaligned
+    assert run(e0=f) == -1                # events: both or neither
+    assert run(wsb=n.value) == -4         # the plain workspace is too small for the prompt pass
+    assert run(batch=300) == -1           # beyond max_batch
+    assert run(batch=0) == 0
+    assert lib.rl_decode_attn_grouped_workspace_size(None, ctypes.byref(ng)) == -1
+    lib.rl_decode_attn_destroy(h)
+    st, h32 = create(lib, cfg(num_q_heads=4, num_kv_heads=4, head_dim=64, q_dtype=0, kv_dtype=0, out_dtype=0,
+                              max_pages_per_seq=16))
+    assert st == 0
+    lib.rl_decode_attn_grouped_workspace_size(h32, ctypes.byref(ng))
+    assert run(handle=h32) == -2          # fp32 caches: no grouped path
+    lib.rl_decode_attn_destroy(h32)
