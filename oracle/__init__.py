@@ -8,6 +8,8 @@ no code with the GPU path.
                  softmax over explicitly gathered pages, OpenMP over (sequence, KV head)).
 * `dense_ref`  - an unpaged brute-force NumPy/`math.fsum` reference for tiny inputs,
                  used to pin `run`.
+* `append`     - one decode step's K/V append into the paged cache, with the fp8
+                 per-page scale rule and an E4M3 encoder (NumPy, fp32 decisions).
 """
 from __future__ import annotations
 
