@@ -102,6 +102,57 @@ def copy_reference(args, torch, dev):
           flush=True)
 
 
+def append_bench(args, torch, dev, w, h, ws):
+    """Time the per-step KV append: every sequence writes its last token's K/V rows
+    (seq_lens[b] - 1) for every KV head; fp8 caches also maintain their page scales."""
+    import numpy as np
+    from paper_2607_09207_amd import inputs as I
+    t = I.to_torch(w, dev)
+    rng = np.random.default_rng(5)
+    shape = (w.batch, w.num_kv_heads, w.head_dim)
+    if w.kv_dtype == "f32":
+        kn = torch.from_numpy(rng.standard_normal(shape).astype(np.float32)).to(dev)
+        vn = torch.from_numpy(rng.standard_normal(shape).astype(np.float32)).to(dev)
+    else:
+        kn = torch.from_numpy(I.f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32)).view(np.int16)).view(
+            torch.bfloat16).to(dev)
+        vn = torch.from_numpy(I.f32_to_bf16_bits(rng.standard_normal(shape).astype(np.float32)).view(np.int16)).view(
+            torch.bfloat16).to(dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def call():
+        h.append(kn, vn, t["k_cache"], t["v_cache"], t["block_table"], t["seq_lens"], k_scale=t["k_scale"],
+                 v_scale=t["v_scale"], workspace=ws, stream=stream)
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        call()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    live = int((w.seq_lens > 0).sum())
+    eb_in = 4 if w.kv_dtype == "f32" else 2
+    eb_kv = {"f32": 4, "bf16": 2, "fp8_e4m3fn": 1}[w.kv_dtype]
+    # algorithmic bytes: new rows read, one row written per (sequence, KV head) and K/V,
+    # lengths and block-table entries read; fp8 also reads and writes each page scale
+    alg = live * w.num_kv_heads * 2 * w.head_dim * (eb_in + eb_kv) + 8 * w.batch
+    if w.kv_dtype == "fp8_e4m3fn":
+        alg += live * w.num_kv_heads * 2 * 8
+    achieved = alg / (ms * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": "KV append per decode step (us per call)", "value": round(ms * 1e3, 3), "unit": "us",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": w.kv_dtype, "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim,
+                   "kv_dtype": w.kv_dtype, "rows_written": live * w.num_kv_heads * 2},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 5), "traffic": None},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -111,8 +162,9 @@ def main():
     ap.add_argument("--sets", type=int, default=3, help="KV pool copies rotated across calls")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of CPU oracle work (0 = skip)")
     ap.add_argument("--ranges", type=int, default=0, help="force the number of work ranges (tuning)")
-    ap.add_argument("--mode", choices=["attention", "copy"], default="attention",
-                    help="copy: a plain device copy of --copy-mib MiB, the reference for HBM counter scaling")
+    ap.add_argument("--mode", choices=["attention", "append", "copy"], default="attention",
+                    help="append: the per-step KV append (rl_decode_attn_append) on the workload's last tokens; "
+                         "copy: a plain device copy of --copy-mib MiB, the reference for HBM counter scaling")
     ap.add_argument("--copy-mib", type=int, default=256)
     ap.add_argument("--prompt-tokens", type=int, default=0,
                     help="GRPO workload only: prompt length shared by each group (default 512)")
@@ -146,16 +198,18 @@ def main():
         w = I.grpo_shared_prefix_bf16(prompt_len=args.prompt_tokens)
     else:
         w = I.make_workload(args.workload)
+    strides = None if w.layout == "page_head_slot" else w.strides()
+    h = DecodeAttention(w.num_q_heads, w.num_kv_heads, w.head_dim, w.batch, w.max_pages_per_seq, w.q_dtype,
+                        w.kv_dtype, "f32", kv_head_of_q=w.kv_head_of_q, kv_strides=strides,
+                        num_work_ranges=args.ranges)
+    if args.mode == "append":
+        return append_bench(args, torch, dev, w, h, h.workspace(dev))
     sets = [I.to_torch(w, dev)]
     for _ in range(args.sets - 1):
         s = dict(sets[0])
         s["k_cache"] = sets[0]["k_cache"].clone()
         s["v_cache"] = sets[0]["v_cache"].clone()
         sets.append(s)
-    strides = None if w.layout == "page_head_slot" else w.strides()
-    h = DecodeAttention(w.num_q_heads, w.num_kv_heads, w.head_dim, w.batch, w.max_pages_per_seq, w.q_dtype,
-                        w.kv_dtype, "f32", kv_head_of_q=w.kv_head_of_q, kv_strides=strides,
-                        num_work_ranges=args.ranges)
     out = torch.empty((w.batch, w.num_q_heads, w.head_dim), dtype=torch.float32, device=dev)
     grouped = args.grouped == "on"
     gkw = {}

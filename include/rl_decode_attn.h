@@ -173,6 +173,35 @@ rlda_status rl_decode_attn_run_grouped(rl_decode_attn_t handle, int32_t batch, i
  * for the prompt pass's per-row results (host-only). */
 rlda_status rl_decode_attn_grouped_workspace_size(rl_decode_attn_t handle, size_t* bytes);
 
+/*
+ * Append one decode step's K and V rows to the paged cache: the write that
+ * precedes each step's attention, since every live request adds one token per
+ * step (App. A.1.2, decode steps and the per-token footprint b_kv).  For every
+ * sequence b with 1 <= seq_lens[b] <= max_pages_per_seq*16, token
+ * t = seq_lens[b] - 1 (seq_lens counts the new token, as for rl_decode_attn_run)
+ * is written to slot t % 16 of page block_table[b][t / 16] for every KV head:
+ *   k_new, v_new  [batch][Hkv][d]  q_dtype: bf16 for bf16 and fp8 caches, f32 for f32
+ *   k_cache, v_cache, k_scale, v_scale, block_table, seq_lens: as for rl_decode_attn_run
+ *   (the caches and, for fp8, the scales are written).
+ * bf16 and f32 caches store the rows as given.  fp8 caches keep each (page, KV head)
+ * scale covering every row written so far (the paper fixes no rule; this is the
+ * library's):
+ *   - slot 0 (a new page): scale = amax / 448, amax = the row's largest |value|;
+ *   - a later slot: if amax > 448 * scale, scale = amax / 448 and the page's earlier
+ *     rows are re-encoded, byte = E4M3(decode(byte) * (old scale / new scale)); a
+ *     stored scale that is not positive and finite counts as 0 (earlier rows become 0);
+ *   - the row is stored as E4M3(value / scale), zero bytes when scale is 0;
+ * all in fp32, E4M3 rounding to nearest even and saturating at 448.
+ * The pages one call writes must each belong to one sequence.  A length outside
+ * [0, capacity] or an out-of-pool page id skips that sequence and raises the flag
+ * rl_decode_attn_run would; seq_lens[b] == 0 skips silently.  workspace: as for
+ * rl_decode_attn_run (only its flag word is used).  One kernel, asynchronous.
+ */
+rlda_status rl_decode_attn_append(rl_decode_attn_t handle, int32_t batch, int32_t num_pages, const void* k_new,
+                                  const void* v_new, void* k_cache, void* v_cache, float* k_scale, float* v_scale,
+                                  const int32_t* block_table, const int32_t* seq_lens, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+
 /* Flags raised by device-side contract checks since the workspace was zeroed
  * (bit 0: page id outside [0, num_pages); bit 1: seq_len beyond capacity;
  * bit 2: a group's shared prompt clamped to its shortest member).

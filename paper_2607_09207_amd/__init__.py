@@ -139,6 +139,26 @@ class DecodeAttention:
             _abi.check(self._lib.rl_decode_attn_run_profiled(*args, e0, e1), "rl_decode_attn_run_profiled")
         return out
 
+    def append(self, k_new, v_new, k_cache, v_cache, block_table, seq_lens, k_scale=None, v_scale=None,
+               workspace=None, stream=None, num_pages: Optional[int] = None):
+        """Write one decode step's K/V rows ([B][Hkv][d], the q dtype) into the caches at
+        token seq_lens[b] - 1 of every sequence (rl_decode_attn_append); fp8 caches also
+        update their per-page scales."""
+        torch = _torch()
+        B = int(k_new.shape[0])
+        ws = workspace if workspace is not None else self.workspace(k_new.device)
+        if stream is None:
+            stream = torch.cuda.current_stream(k_new.device).cuda_stream
+        elif hasattr(stream, "cuda_stream"):
+            stream = stream.cuda_stream
+        npages = int(k_cache.shape[0]) if num_pages is None else int(num_pages)
+        ptr = lambda t: None if t is None else t.data_ptr()
+        wp = self._aligned_ptr(ws)
+        _abi.check(self._lib.rl_decode_attn_append(self._h, B, npages, ptr(k_new), ptr(v_new), ptr(k_cache),
+                                                   ptr(v_cache), ptr(k_scale), ptr(v_scale), ptr(block_table),
+                                                   ptr(seq_lens), wp, ws.numel() - (wp - ws.data_ptr()), stream),
+                   "rl_decode_attn_append")
+
     def read_flags(self, workspace=None, device=None, stream=None) -> int:
         torch = _torch()
         ws = workspace if workspace is not None else self.workspace(device)

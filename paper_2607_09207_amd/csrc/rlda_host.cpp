@@ -291,6 +291,50 @@ rlda_status rl_decode_attn_run_grouped(rl_decode_attn_t h, int32_t batch, int32_
                   block_table, seq_lens, out, workspace, workspace_bytes, stream, event_begin, event_end);
 }
 
+rlda_status rl_decode_attn_append(rl_decode_attn_t h, int32_t batch, int32_t num_pages, const void* k_new,
+                                  const void* v_new, void* k_cache, void* v_cache, float* k_scale, float* v_scale,
+                                  const int32_t* block_table, const int32_t* seq_lens, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  if (!h) return RLDA_ERR_INVALID_ARG;
+  const rl_decode_attn_config& c = h->cfg;
+  if (batch < 0 || batch > c.max_batch || num_pages < 0) return RLDA_ERR_INVALID_ARG;
+  if (batch == 0) return RLDA_OK;
+  if (!k_new || !v_new || !block_table || !seq_lens) return RLDA_ERR_INVALID_ARG;
+  if (num_pages > 0 && (!k_cache || !v_cache)) return RLDA_ERR_INVALID_ARG;
+  if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_cache) || !aligned16(v_cache))
+    return RLDA_ERR_INVALID_ARG;
+  if (((uintptr_t)block_table & 3u) || ((uintptr_t)seq_lens & 3u)) return RLDA_ERR_INVALID_ARG;
+  if (h->kind == rlda::KvKind::FP8 && num_pages > 0 &&
+      (!k_scale || !v_scale || ((uintptr_t)k_scale & 3u) || ((uintptr_t)v_scale & 3u)))
+    return RLDA_ERR_INVALID_ARG;
+  const WsLayout wl = layout_of(h);
+  if (!workspace || ((uintptr_t)workspace % kAlign)) return RLDA_ERR_WORKSPACE;
+  if (workspace_bytes < wl.total) return RLDA_ERR_WORKSPACE;
+  rlda::Params p;
+  memset(&p, 0, sizeof p);
+  p.k = k_cache;
+  p.v = v_cache;
+  p.k_scale = k_scale;
+  p.v_scale = v_scale;
+  p.k_in = k_new;
+  p.v_in = v_new;
+  p.block_table = block_table;
+  p.seq_lens = seq_lens;
+  p.flags = (uint32_t*)((char*)workspace + wl.flags);
+  const int eb = elem_bytes(c.kv_dtype);
+  p.stride_page = h->stride_page * eb;
+  p.stride_head = h->stride_head * eb;
+  p.stride_slot = (int32_t)(h->stride_slot * eb);
+  p.batch = batch;
+  p.num_pages = num_pages;
+  p.num_q_heads = c.num_q_heads;
+  p.num_kv_heads = c.num_kv_heads;
+  p.group = h->group;
+  p.max_pages = c.max_pages_per_seq;
+  if (rlda::launch_append(h->kind, c.head_dim, p, stream) != hipSuccess) return RLDA_ERR_HIP;
+  return RLDA_OK;
+}
+
 rlda_status rl_decode_attn_read_flags(rl_decode_attn_t h, const void* workspace, void* stream, uint32_t* flags) {
   if (!h || !workspace || !flags) return RLDA_ERR_INVALID_ARG;
   uint32_t v = 0;

@@ -1129,6 +1129,108 @@ void prompt_kernel(const Params p) {
   if ((tid & 3) == 0) *(f32x2*)(p.pfx_ml + orow * 2) = f32x2{M, Ls};
 }
 
+// ---------------------------------------------------------------- KV append
+// One wave per (sequence, KV head): lane l owns elements [l * E, (l + 1) * E) of a
+// row, E = D / 64.  bf16 / fp32 caches copy the new row into its slot.  fp8 caches
+// keep the page's scale covering every row written so far: the first row of a page
+// sets amax / 448; a later row with a larger amax raises the scale and re-encodes
+// the earlier rows (decode, times old/new scale, round to nearest even).
+
+// E4M3 (OCP FN) encoding of two fp32 values into the low 16 bits, round to nearest even.
+__device__ __forceinline__ uint32_t e4m3x2(float a, float b) {
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false) & 0xFFFFu;
+}
+
+template <int D, KvKind KIND>
+__global__ __launch_bounds__(kThreads) void append_kernel(const Params p) {
+  constexpr int E = D / 64;
+  const int lane = threadIdx.x & 63;
+  const int item = uni((int)(blockIdx.x * kWaves + (threadIdx.x >> 6)));
+  if (item >= p.batch * p.num_kv_heads) return;
+  const int b = item / p.num_kv_heads, g = item - b * p.num_kv_heads;
+  const int cap = p.max_pages * kPage;
+  const int L = uni(p.seq_lens[b]);
+  if (L < 1 || L > cap) {
+    if ((L < 0 || L > cap) && lane == 0) atomicOr(p.flags, kFlagBadLen);
+    return;
+  }
+  const int t = L - 1, slot = t % kPage;
+  const int pid = uni(p.block_table[(int64_t)b * p.max_pages + t / kPage]);
+  if ((unsigned)pid >= (unsigned)p.num_pages) {
+    if (lane == 0) atomicOr(p.flags, kFlagBadPage);
+    return;
+  }
+  const int64_t row0 = (int64_t)pid * p.stride_page + (int64_t)g * p.stride_head;   // bytes, slot 0
+  const int64_t in_off = ((int64_t)item * D + lane * E);                               // elements
+
+#pragma unroll
+  for (int kv = 0; kv < 2; ++kv) {
+    char* cache = (char*)(kv ? p.v : p.k);
+    const void* in = kv ? p.v_in : p.k_in;
+    if constexpr (KIND == KvKind::F32) {
+      const float* src = (const float*)in + in_off;
+      float* dst = (float*)(cache + row0 + (int64_t)slot * p.stride_slot) + lane * E;
+#pragma unroll
+      for (int e = 0; e < E; ++e) dst[e] = src[e];
+    } else if constexpr (KIND == KvKind::BF16) {
+      const uint16_t* src = (const uint16_t*)in + in_off;
+      uint16_t* dst = (uint16_t*)(cache + row0 + (int64_t)slot * p.stride_slot) + lane * E;
+#pragma unroll
+      for (int e = 0; e < E; ++e) dst[e] = src[e];
+    } else {
+      float* scales = (float*)(kv ? p.v_scale : p.k_scale);
+      const uint16_t* src = (const uint16_t*)in + in_off;
+      float x[E];
+      float amax = 0.f;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        x[e] = __uint_as_float((uint32_t)src[e] << 16);
+        amax = fmaxf(amax, fabsf(x[e]));
+      }
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) amax = fmaxf(amax, __shfl_xor(amax, o));
+      amax = __builtin_bit_cast(float, uni(__builtin_bit_cast(int, amax)));
+      const int64_t si = (int64_t)pid * p.num_kv_heads + g;
+      float s = 0.f;
+      if (slot > 0) {
+        s = scales[si];
+        if (!(s > 0.f) || __builtin_isinf(s)) s = 0.f;
+      }
+      float s_new = s;
+      if (slot == 0 || amax > 448.f * s) {
+        s_new = amax / 448.f;
+        // Earlier rows of the page (slot > 0 only): re-encode at the new scale.
+        const float ratio = s > 0.f ? s / s_new : 0.f;
+        for (int r = 0; r < slot; ++r) {
+          uint8_t* rp = (uint8_t*)(cache + row0 + (int64_t)r * p.stride_slot) + lane * E;
+          if constexpr (E == 2) {
+            const uint32_t w = *(const uint16_t*)rp;
+            const f32x2 v = fp8x2_to_f32(w, false);
+            *(uint16_t*)rp = (uint16_t)(s > 0.f ? e4m3x2(v[0] * ratio, v[1] * ratio) : 0u);
+          } else {
+            const f32x2 v = fp8x2_to_f32((uint32_t)*rp, false);
+            *rp = (uint8_t)(s > 0.f ? e4m3x2(v[0] * ratio, 0.f) & 0xFFu : 0u);
+          }
+        }
+      }
+      uint8_t* dst = (uint8_t*)(cache + row0 + (int64_t)slot * p.stride_slot) + lane * E;
+      if constexpr (E == 2)
+        *(uint16_t*)dst = (uint16_t)(s_new > 0.f ? e4m3x2(x[0] / s_new, x[1] / s_new) : 0u);
+      else
+        *dst = (uint8_t)(s_new > 0.f ? e4m3x2(x[0] / s_new, 0.f) & 0xFFu : 0u);
+      if (lane == 0) scales[si] = s_new;
+    }
+  }
+}
+
+template <int D, KvKind KIND>
+int launch_append_t(const Params& p, void* stream) {
+  const int items = p.batch * p.num_kv_heads;
+  hipLaunchKernelGGL((append_kernel<D, KIND>), dim3((items + kWaves - 1) / kWaves), dim3(kThreads), 0,
+                     (hipStream_t)stream, p);
+  return (int)hipGetLastError();
+}
+
 template <class Pol>
 int launch(const Params& p, void* stream, void* ev_begin, void* ev_end) {
   hipStream_t st = (hipStream_t)stream;
@@ -1170,6 +1272,18 @@ int launch_prompt_then_decode(const Params& p, int ngroups, void* stream, void* 
 int launch_decode(KvKind kind, int head_dim, int group, const Params& p, void* stream, void* ev_begin,
                   void* ev_end) {
   RLDA_DISPATCH(launch, p, stream, ev_begin, ev_end)
+}
+
+int launch_append(KvKind kind, int head_dim, const Params& p, void* stream) {
+  switch (kind) {
+    case KvKind::BF16:
+      return head_dim == 128 ? launch_append_t<128, KvKind::BF16>(p, stream) : launch_append_t<64, KvKind::BF16>(p, stream);
+    case KvKind::FP8:
+      return head_dim == 128 ? launch_append_t<128, KvKind::FP8>(p, stream) : launch_append_t<64, KvKind::FP8>(p, stream);
+    case KvKind::F32:
+      return head_dim == 128 ? launch_append_t<128, KvKind::F32>(p, stream) : launch_append_t<64, KvKind::F32>(p, stream);
+  }
+  return -1;
 }
 
 int launch_grouped(KvKind kind, int head_dim, int, const Params& p, int ngroups, void* stream, void* ev_begin,

@@ -52,6 +52,9 @@ struct Params {
   int32_t pfx_nblocks;         // jobs per (group, KV head)
   int32_t pfx_splits;          // workgroups per job (their states meet in the partial slots)
   int32_t pfx_slots;           // capacity of part_acc / part_ml in 64-row prompt-pass slots
+  // KV append (rl_decode_attn_append): the step's new rows, [batch][Hkv][D] in the q dtype.
+  const void* k_in;
+  const void* v_in;
   int16_t q_head[kMaxQHeads];  // q_head[g * G + i] = i-th query head of KV head g
 };
 
@@ -65,5 +68,7 @@ int launch_decode(KvKind kind, int head_dim, int group, const Params& p, void* s
 // followed by the attention kernel.
 int launch_grouped(KvKind kind, int head_dim, int group, const Params& p, int ngroups, void* stream,
                    void* ev_begin, void* ev_end);
+// KV append: one wave per (sequence, KV head).
+int launch_append(KvKind kind, int head_dim, const Params& p, void* stream);
 
 }  // namespace rlda

@@ -183,3 +183,27 @@ def test_grouped_run_rejects_bad_arguments_before_launch(lib):
     lib.rl_decode_attn_grouped_workspace_size(h32, ctypes.byref(ng))
     assert run(handle=h32) == -2          # fp32 caches: no grouped path
     lib.rl_decode_attn_destroy(h32)
+
+
+def test_append_rejects_bad_arguments_before_launch(lib):
+    st, h = create(lib, cfg(kv_dtype=_abi.RLDA_FP8_E4M3FN))
+    assert st == 0
+    n = ctypes.c_size_t()
+    lib.rl_decode_attn_workspace_size(h, ctypes.byref(n))
+    f = 0x10000
+
+    def app(batch=4, kn=f, vn=f, kc=f, vc=f, ks=f, vs=f, bt=f, sl=f, ws=f * 16, wsb=None):
+        return lib.rl_decode_attn_append(h, batch, 10, kn, vn, kc, vc, ks, vs, bt, sl, ws,
+                                         n.value if wsb is None else wsb, None)
+
+    assert app(kn=None) == -1
+    assert app(vn=f + 2) == -1            # misaligned rows
+    assert app(kc=None) == -1
+    assert app(ks=None) == -1             # fp8 needs scales
+    assert app(sl=f + 1) == -1
+    assert app(batch=65) == -1
+    assert app(ws=None) == -4
+    assert app(wsb=n.value - 1) == -4
+    assert app(batch=0) == 0
+    assert lib.rl_decode_attn_append(None, 1, 1, *([f] * 8), f, 1, None) == -1
+    lib.rl_decode_attn_destroy(h)
