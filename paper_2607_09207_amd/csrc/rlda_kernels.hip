@@ -198,16 +198,12 @@ __device__ __forceinline__ void lse_merge(float& M, float& Ls, float* o, float m
 // Merge the pieces of segment (b, g) held by workgroups u_first..u_last: the piece
 // of workgroup k is in slot 2k+1 when it continues past k's share, else in slot 2k.
 // Loads are issued kBatch pieces at a time (one round trip per batch), then merged
-// in piece order with a running maximum.  Thread (h, d0) writes its D/16 outputs.
-template <int D>
-__device__ __forceinline__ void merge_pieces(const Params& p, int b, int g, int h, int d0, int64_t u_first,
-                                             int64_t u_last) {
-  constexpr int DPT = D / 16, kBatch = 4;
+// in piece order with a running maximum.  Thread (h, d0) merges its D/16 outputs.
+template <int D, int kBatch>
+__device__ __forceinline__ void merge_batches(const Params& p, const PartialRsrc& rs, int h, int d0, int64_t u_first,
+                                              int64_t u_last, float& M, float& Ls, float* o) {
+  constexpr int DPT = D / 16;
   const int G = p.group;
-  const PartialRsrc rs = PartialRsrc::of<D>(p);
-  float M = neg_inf(), Ls = 0.f, o[DPT];
-#pragma unroll
-  for (int e = 0; e < DPT; ++e) o[e] = 0.f;
   for (int64_t k0 = u_first; k0 <= u_last; k0 += kBatch) {
     u32x2 ml[kBatch];
     float v[kBatch][DPT];
@@ -226,7 +222,23 @@ __device__ __forceinline__ void merge_pieces(const Params& p, int b, int g, int 
       if (k0 + i <= u_last)
         lse_merge<DPT>(M, Ls, o, __uint_as_float(ml[i][0]), __uint_as_float(ml[i][1]), v[i]);
   }
-  store_out<D>(p, b, s_qhead[g * G + h], d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
+}
+
+// A segment cut into many pieces (a long sequence over few workgroups' worth of
+// other work) is merged 16 pieces per round trip; the common 2-4 pieces, 4 at a time.
+template <int D>
+__device__ __forceinline__ void merge_pieces(const Params& p, int b, int g, int h, int d0, int64_t u_first,
+                                             int64_t u_last) {
+  constexpr int DPT = D / 16;
+  const PartialRsrc rs = PartialRsrc::of<D>(p);
+  float M = neg_inf(), Ls = 0.f, o[DPT];
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) o[e] = 0.f;
+  if (u_last - u_first >= 4)
+    merge_batches<D, 16>(p, rs, h, d0, u_first, u_last, M, Ls, o);
+  else
+    merge_batches<D, 4>(p, rs, h, d0, u_first, u_last, M, Ls, o);
+  store_out<D>(p, b, s_qhead[g * p.group + h], d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
 }
 
 // ---------------------------------------------------------------- MFMA policy
