@@ -64,3 +64,35 @@ def dense_decode_attention(w, scale: float = 0.0) -> np.ndarray:
             p = np.array([x / z for x in e])
             out[b, h] = [math.fsum(p * Vd[:, j]) for j in range(d)]
     return out
+
+
+def dense_multi_query_attention(w, scale: float = 0.0) -> np.ndarray:
+    """Multi-token queries ([total_q][Hq][d], rows of sequence b from w.q_start):
+    all scores of a query row against every cached token of its sequence, then an
+    explicit causal mask (token t is visible to the sequence's query i of n when
+    t <= L - n + i), softmax over the visible entries."""
+    Hq, d, P = w.num_q_heads, w.head_dim, w.page_size
+    qd = decode_array(w.q, w.q_dtype)
+    K, V = dense_pages(w, "k"), dense_pages(w, "v")
+    sc = scale if scale > 0 else 1.0 / math.sqrt(d)
+    qs = np.asarray(w.q_start, np.int64)
+    out = np.zeros((int(qs[-1]), Hq, d), np.float64)
+    for b in range(w.batch):
+        L, n = int(w.seq_lens[b]), int(qs[b + 1] - qs[b])
+        if n == 0:
+            continue
+        npg = -(-L // P)
+        pages = w.block_table[b, :npg]
+        visible = np.arange(L)[None, :] <= (L - n + np.arange(n))[:, None]     # [n][L]
+        for h in range(Hq):
+            g = int(w.kv_head_of_q[h])
+            Kd = np.take(K[:, g], pages, axis=0).reshape(npg * P, d)[:L]
+            Vd = np.take(V[:, g], pages, axis=0).reshape(npg * P, d)[:L]
+            for i in range(n):
+                s = [sc * math.fsum(qd[qs[b] + i, h] * Kd[t]) for t in range(L)]
+                m = max(s[t] for t in range(L) if visible[i, t])
+                e = [math.exp(s[t] - m) if visible[i, t] else 0.0 for t in range(L)]
+                z = math.fsum(e)
+                p = np.array([x / z for x in e])
+                out[qs[b] + i, h] = [math.fsum(p * Vd[:, j]) for j in range(d)]
+    return out

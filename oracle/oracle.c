@@ -24,6 +24,20 @@
  * explicit gather of every token through the block table, all scores, the row
  * maximum, exponentials, their sum, then the weighted sum of V - two passes over
  * the tokens in ascending order, no splitting, no online rescaling.
+ *
+ * Multi-token queries.  Rollout also runs prefill over prompt tokens before it
+ * decodes (Sec. 3, rollout; App. A.1.2, the prefill cost whose attention term
+ * grows with the square of the prompt length).  A prefill chunk of n_b tokens of
+ * sequence b sits at the end of its seq_lens[b] cached tokens (their K/V already
+ * written); its query token i (0 <= i < n_b) is at position
+ * pos = seq_lens[b] - n_b + i and attends causally to positions 0 .. pos:
+ *
+ *     o[r,h,:] = sum_{t <= pos} softmax_t( scale * q[r,h,:] . k_t ) * v_t,
+ *     r = q_start[b] + i,
+ *
+ * i.e. the decode definition above with history pos + 1.  Decode is the case
+ * n_b = 1.  oracle_multi_query_attention evaluates exactly that, one query token
+ * at a time, with the same two-pass routine.
  */
 #include <math.h>
 #include <omp.h>
@@ -38,7 +52,8 @@ enum {
   ORC_BAD_ARG = -1,
   ORC_BAD_LEN = -2,
   ORC_BAD_PAGE = -3,
-  ORC_NO_MEM = -4
+  ORC_NO_MEM = -4,
+  ORC_BAD_QLEN = -5
 };
 
 /* bf16: the upper 16 bits of an IEEE binary32. */
@@ -94,17 +109,19 @@ typedef struct {
   double* out;
 } orc_args;
 
-/* One (sequence b, KV head g): every query head h with kv_head_of_q[h] == g. */
-static int orc_one(const orc_args* a, int b, int g, double* kbuf, double* vbuf, double* s, int* heads) {
+/* One (sequence b, KV head g): every query head h with kv_head_of_q[h] == g
+ * attends to the first L tokens of sequence b; its query and output are row
+ * `row` of q and out ([row][num_q_heads][head_dim]). */
+static int orc_one(const orc_args* a, int b, int g, int L, int64_t row, double* kbuf, double* vbuf, double* s,
+                   int* heads) {
   const int d = a->head_dim, P = a->page_size;
-  const int L = a->seq_lens[b];
   int nh = 0;
   for (int h = 0; h < a->num_q_heads; ++h)
     if (a->kv_head_of_q[h] == g) heads[nh++] = h;
 
   if (L == 0) {
     for (int i = 0; i < nh; ++i)
-      for (int j = 0; j < d; ++j) a->out[((int64_t)b * a->num_q_heads + heads[i]) * d + j] = 0.0;
+      for (int j = 0; j < d; ++j) a->out[(row * a->num_q_heads + heads[i]) * d + j] = 0.0;
     return ORC_OK;
   }
 
@@ -117,7 +134,7 @@ static int orc_one(const orc_args* a, int b, int g, double* kbuf, double* vbuf, 
     double ks = (a->kv_dtype == ORC_FP8_E4M3FN) ? (double)a->k_scale[(int64_t)pid * a->num_kv_heads + g] : 1.0;
     for (int j = 0; j < d; ++j) kbuf[j] = orc_load(a->k_cache, a->kv_dtype, base + j) * ks;
     for (int i = 0; i < nh; ++i) {
-      int64_t qb = ((int64_t)b * a->num_q_heads + heads[i]) * d;
+      int64_t qb = (row * a->num_q_heads + heads[i]) * d;
       double dot = 0.0;
       for (int j = 0; j < d; ++j) dot += orc_load(a->q, a->q_dtype, qb + j) * kbuf[j];
       s[(int64_t)i * L + t] = a->scale * dot;
@@ -134,7 +151,7 @@ static int orc_one(const orc_args* a, int b, int g, double* kbuf, double* vbuf, 
 
   /* Pass 2: out = sum_t w_t v_t / Z. */
   for (int i = 0; i < nh; ++i) {
-    double* o = a->out + ((int64_t)b * a->num_q_heads + heads[i]) * d;
+    double* o = a->out + (row * a->num_q_heads + heads[i]) * d;
     for (int j = 0; j < d; ++j) o[j] = 0.0;
   }
   for (int t = 0; t < L; ++t) {
@@ -145,7 +162,7 @@ static int orc_one(const orc_args* a, int b, int g, double* kbuf, double* vbuf, 
     for (int j = 0; j < d; ++j) vbuf[j] = orc_load(a->v_cache, a->kv_dtype, base + j) * vs;
     for (int i = 0; i < nh; ++i) {
       double w = s[(int64_t)i * L + t];
-      double* o = a->out + ((int64_t)b * a->num_q_heads + heads[i]) * d;
+      double* o = a->out + (row * a->num_q_heads + heads[i]) * d;
       for (int j = 0; j < d; ++j) o[j] += w * vbuf[j];
     }
   }
@@ -153,13 +170,13 @@ static int orc_one(const orc_args* a, int b, int g, double* kbuf, double* vbuf, 
     double z = 0.0;
     const double* si = s + (int64_t)i * L;
     for (int t = 0; t < L; ++t) z += si[t];
-    double* o = a->out + ((int64_t)b * a->num_q_heads + heads[i]) * d;
+    double* o = a->out + (row * a->num_q_heads + heads[i]) * d;
     for (int j = 0; j < d; ++j) o[j] /= z;
   }
   return ORC_OK;
 }
 
-typedef struct { int b, g, L; } orc_unit;
+typedef struct { int b, g, L; int64_t row; } orc_unit;
 
 static int orc_longest_first(const void* x, const void* y) {
   const orc_unit* u = (const orc_unit*)x;
@@ -167,6 +184,34 @@ static int orc_longest_first(const void* x, const void* y) {
   if (u->L != v->L) return v->L - u->L;
   if (u->b != v->b) return u->b - v->b;
   return u->g - v->g;
+}
+
+/* Evaluate every unit (longest first, dynamic schedule); the first failure wins. */
+static int orc_run_units(const orc_args* ap, orc_unit* units, int nunits, int maxL, int num_threads) {
+  const orc_args a = *ap;
+  const int head_dim = a.head_dim, num_q_heads = a.num_q_heads;
+  qsort(units, (size_t)nunits, sizeof(orc_unit), orc_longest_first);
+
+  int status = ORC_OK;
+  if (num_threads <= 0) num_threads = omp_get_max_threads();
+  #pragma omp parallel num_threads(num_threads)
+  {
+    double* kbuf = (double*)malloc(sizeof(double) * (size_t)head_dim);
+    double* vbuf = (double*)malloc(sizeof(double) * (size_t)head_dim);
+    double* s = (double*)malloc(sizeof(double) * (size_t)num_q_heads * (size_t)(maxL > 0 ? maxL : 1));
+    int* heads = (int*)malloc(sizeof(int) * (size_t)num_q_heads);
+    int local = (kbuf && vbuf && s && heads) ? ORC_OK : ORC_NO_MEM;
+    #pragma omp for schedule(dynamic, 1)
+    for (int u = 0; u < nunits; ++u) {
+      if (local != ORC_OK) continue;
+      int r = orc_one(&a, units[u].b, units[u].g, units[u].L, units[u].row, kbuf, vbuf, s, heads);
+      if (r != ORC_OK) local = r;
+    }
+    #pragma omp critical
+    { if (local != ORC_OK) status = local; }
+    free(kbuf); free(vbuf); free(s); free(heads);
+  }
+  return status;
 }
 
 /*
@@ -206,29 +251,68 @@ int oracle_decode_attention(int batch, int num_q_heads, int num_kv_heads, int he
   if (!units) return ORC_NO_MEM;
   for (int b = 0; b < batch; ++b) {
     if (batch_mask && !batch_mask[b]) continue;
-    for (int g = 0; g < num_kv_heads; ++g) units[nunits++] = (orc_unit){b, g, seq_lens[b]};
+    for (int g = 0; g < num_kv_heads; ++g) units[nunits++] = (orc_unit){b, g, seq_lens[b], b};
   }
-  qsort(units, (size_t)nunits, sizeof(orc_unit), orc_longest_first);
+  int status = orc_run_units(&a, units, nunits, maxL, num_threads);
+  free(units);
+  return status;
+}
 
-  int status = ORC_OK;
-  if (num_threads <= 0) num_threads = omp_get_max_threads();
-  #pragma omp parallel num_threads(num_threads)
-  {
-    double* kbuf = (double*)malloc(sizeof(double) * (size_t)head_dim);
-    double* vbuf = (double*)malloc(sizeof(double) * (size_t)head_dim);
-    double* s = (double*)malloc(sizeof(double) * (size_t)num_q_heads * (size_t)(maxL > 0 ? maxL : 1));
-    int* heads = (int*)malloc(sizeof(int) * (size_t)num_q_heads);
-    int local = (kbuf && vbuf && s && heads) ? ORC_OK : ORC_NO_MEM;
-    #pragma omp for schedule(dynamic, 1)
-    for (int u = 0; u < nunits; ++u) {
-      if (local != ORC_OK) continue;
-      int r = orc_one(&a, units[u].b, units[u].g, kbuf, vbuf, s, heads);
-      if (r != ORC_OK) local = r;
-    }
-    #pragma omp critical
-    { if (local != ORC_OK) status = local; }
-    free(kbuf); free(vbuf); free(s); free(heads);
+/*
+ * Multi-token queries: compute out[r][h][:] (fp64, [total_q][num_q_heads][head_dim])
+ * for every query row r = q_start[b] + i, 0 <= i < n_b = q_start[b+1] - q_start[b],
+ * of every b with batch_mask == NULL or batch_mask[b] != 0; q is
+ * [total_q][num_q_heads][head_dim] with total_q = q_start[batch].  Row r attends
+ * causally to the first seq_lens[b] - n_b + i + 1 tokens of sequence b.  Rows of
+ * other sequences are untouched.  Returns ORC_BAD_QLEN when q_start is not
+ * non-decreasing from 0 or a selected sequence has more query tokens than cached
+ * tokens, otherwise as oracle_decode_attention.
+ */
+int oracle_multi_query_attention(int batch, int num_q_heads, int num_kv_heads, int head_dim, int page_size,
+                                 int max_pages_per_seq, int num_pages, int q_dtype, int kv_dtype, const void* q,
+                                 const void* k_cache, const void* v_cache, const float* k_scale,
+                                 const float* v_scale, int64_t stride_page, int64_t stride_head,
+                                 int64_t stride_slot, const int32_t* block_table, const int32_t* seq_lens,
+                                 const int32_t* q_start, const int32_t* kv_head_of_q, double scale,
+                                 const uint8_t* batch_mask, double* out, int num_threads) {
+  if (batch < 0 || num_q_heads <= 0 || num_kv_heads <= 0 || head_dim <= 0 || page_size <= 0) return ORC_BAD_ARG;
+  if (q_dtype != ORC_F32 && q_dtype != ORC_BF16) return ORC_BAD_ARG;
+  if (kv_dtype < ORC_F32 || kv_dtype > ORC_FP8_E4M3FN) return ORC_BAD_ARG;
+  if (kv_dtype == ORC_FP8_E4M3FN && (!k_scale || !v_scale)) return ORC_BAD_ARG;
+  for (int h = 0; h < num_q_heads; ++h)
+    if (kv_head_of_q[h] < 0 || kv_head_of_q[h] >= num_kv_heads) return ORC_BAD_ARG;
+  if (q_start[0] != 0) return ORC_BAD_QLEN;
+  int64_t nunits_all = 0;
+  int maxL = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int n = q_start[b + 1] - q_start[b];
+    if (n < 0) return ORC_BAD_QLEN;
+    if (batch_mask && !batch_mask[b]) continue;
+    if (seq_lens[b] < 0 || (int64_t)seq_lens[b] > (int64_t)max_pages_per_seq * page_size) return ORC_BAD_LEN;
+    if (n > seq_lens[b]) return ORC_BAD_QLEN;
+    if (seq_lens[b] > maxL) maxL = seq_lens[b];
+    nunits_all += (int64_t)n * num_kv_heads;
   }
+
+  orc_args a = {batch, num_q_heads, num_kv_heads, head_dim, page_size, max_pages_per_seq, num_pages,
+                q_dtype, kv_dtype, q, k_cache, v_cache, k_scale, v_scale, stride_page, stride_head,
+                stride_slot, block_table, seq_lens, kv_head_of_q,
+                scale > 0.0 ? scale : 1.0 / sqrt((double)head_dim), out};
+
+  /* One unit per (query token, KV head): the decode definition with history pos + 1. */
+  if (nunits_all > 0x7fffffff) return ORC_BAD_ARG;
+  orc_unit* units = (orc_unit*)malloc(sizeof(orc_unit) * (size_t)(nunits_all > 0 ? nunits_all : 1));
+  if (!units) return ORC_NO_MEM;
+  int nunits = 0;
+  for (int b = 0; b < batch; ++b) {
+    if (batch_mask && !batch_mask[b]) continue;
+    const int n = q_start[b + 1] - q_start[b];
+    for (int i = 0; i < n; ++i) {
+      const int pos = seq_lens[b] - n + i;
+      for (int g = 0; g < num_kv_heads; ++g) units[nunits++] = (orc_unit){b, g, pos + 1, (int64_t)q_start[b] + i};
+    }
+  }
+  int status = orc_run_units(&a, units, nunits, maxL, num_threads);
   free(units);
   return status;
 }

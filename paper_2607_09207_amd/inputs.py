@@ -16,6 +16,9 @@ Layouts (all row-major):
   k/v scale    [NP][Hkv]           fp32, fp8 caches only; real value = decode(byte) * scale
   block_table  [B][MP]             int32 page ids, -1 past the sequence's last page
   seq_lens     [B]                 int32, cached tokens including the current one
+  q_start      [B + 1]             multi-token queries only: sequence b's query rows are
+                                   q[q_start[b] : q_start[b+1]] (q is then [total_q][Hq][d]),
+                                   its last q_start[b+1] - q_start[b] cached tokens
 Token t of sequence b lives in page block_table[b][t // P], slot t % P.  Slots past
 the sequence end in its last page, and pool pages no sequence references, are filled
 with NaN so that any read of them shows up in the output.
@@ -127,6 +130,7 @@ class Workload:
     shared_prefix_tokens: int = 0         # GRPO: prompt tokens shared by a group
     group_size: int = 1                   # GRPO: responses per prompt
     seed: int = 0
+    q_start: Optional[np.ndarray] = None  # multi-token queries: [B + 1] row offsets into q
 
     @property
     def num_pages(self) -> int:
@@ -332,6 +336,48 @@ def staleness_mix_bf16(seed=1004):
     return _scattered("staleness_mix_bf16", seed, rng, lens, 64, 8, 128, "bf16", "bf16", 2048)
 
 
+def with_query_rows(w: Workload, q_lens: Sequence[int], seed: Optional[int] = None) -> Workload:
+    """Multi-token version of `w`: sequence b gets q_lens[b] query rows (its last
+    q_lens[b] cached tokens, a prefill chunk), drawn from the same seeded stream."""
+    ql = np.asarray(q_lens, np.int64)
+    assert ql.shape == (w.batch,) and np.all(ql >= 0)
+    qs = np.zeros(w.batch + 1, np.int32)
+    qs[1:] = np.cumsum(ql)
+    q = _gen_q(w.q_dtype, w.seed if seed is None else seed, int(qs[-1]), w.num_q_heads, w.head_dim)
+    return dataclasses.replace(w, q=q, q_start=qs)
+
+
+def make_multi(seq_lens: Sequence[int], q_lens: Sequence[int], num_q_heads: int, num_kv_heads: int,
+               head_dim: int, **kw) -> Workload:
+    """Small multi-token workload: make_custom's cache plus q_lens[b] query rows per sequence."""
+    return with_query_rows(make_custom(seq_lens, num_q_heads, num_kv_heads, head_dim, **kw), q_lens)
+
+
+def prompt_prefill_grpo_bf16(seed=1005):
+    """Prefill of the 32 GRPO prompts: 32 sequences of 512 tokens, each all query
+    rows (a whole prompt, causal), 12 query / 2 KV heads, d=128, bf16; pages scattered."""
+    rng = np.random.default_rng(seed)
+    lens = np.full(32, 512, np.int64)
+    w = _scattered("prompt_prefill_grpo_bf16", seed, rng, lens, 12, 2, 128, "bf16", "bf16", 32)
+    return with_query_rows(w, lens)
+
+
+def chunked_prefill_gqa_bf16(seed=1006, chunk=512):
+    """Chunked prefill on the long-tail GQA cache: 64 sequences, 28 query / 4 KV
+    heads, d=128, bf16, total lengths lognormal (median 2048, sigma 1.0) clipped to
+    [32, 16384]; each sequence's last min(chunk, L) tokens are the chunk's query rows."""
+    rng = np.random.default_rng(seed)
+    lens = _lognormal_lengths(rng, 64, 2048, 1.0, 32, 16384)
+    w = _scattered("chunked_prefill_gqa_bf16", seed, rng, lens, 28, 4, 128, "bf16", "bf16", 1024)
+    return with_query_rows(w, np.minimum(lens, chunk))
+
+
+MULTI_WORKLOADS = {
+    "prompt_prefill_grpo_bf16": prompt_prefill_grpo_bf16,
+    "chunked_prefill_gqa_bf16": chunked_prefill_gqa_bf16,
+}
+
+
 WORKLOADS = {
     "tiny_f32": tiny_f32,
     "gqa_longtail_bf16": gqa_longtail_bf16,
@@ -343,7 +389,7 @@ WORKLOAD_ORDER = list(WORKLOADS)
 
 
 def make_workload(name: str, seed: Optional[int] = None) -> Workload:
-    fn = WORKLOADS[name]
+    fn = WORKLOADS[name] if name in WORKLOADS else MULTI_WORKLOADS[name]
     return fn() if seed is None else fn(seed)
 
 

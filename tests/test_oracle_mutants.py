@@ -1,7 +1,8 @@
 """The oracle's pins must reject plausible mistakes.
 
 Each case plants one mistake in a temporary copy of oracle.c (on the CPU), builds
-it, and runs the pin suite against it; at least one pin must fail.
+it, and runs the pin suite against it (the decode pins, or the multi-token pins for
+mistakes in the multi-token entry point); at least one pin must fail.
 """
 import os
 import shutil
@@ -25,7 +26,13 @@ MUTANTS = {
     "dropped_last_token": ("for (int t = 0; t < L; ++t) {\n    int pid = a->block_table[(int64_t)b * a->max_pages_per_seq + t / P];\n    int slot = t % P;\n    int64_t base",
                            "for (int t = 0; t < L - 1; ++t) {\n    int pid = a->block_table[(int64_t)b * a->max_pages_per_seq + t / P];\n    int slot = t % P;\n    int64_t base"),
     "bf16_low_half": ("uint32_t u = (uint32_t)bits << 16;", "uint32_t u = (uint32_t)bits << 15;"),
+    # multi-token queries
+    "causal_limit_one_early": ("const int pos = seq_lens[b] - n + i;", "const int pos = seq_lens[b] - n + i - 1;"),
+    "causal_limit_one_late": ("(orc_unit){b, g, pos + 1,", "(orc_unit){b, g, pos + 2 > seq_lens[b] ? pos + 1 : pos + 2,"),
+    "query_rows_reversed": ("(int64_t)q_start[b] + i}", "(int64_t)q_start[b] + (n - 1 - i)}"),
+    "chunk_at_sequence_start": ("const int pos = seq_lens[b] - n + i;", "const int pos = i;"),
 }
+MULTI = {"causal_limit_one_early", "causal_limit_one_late", "query_rows_reversed", "chunk_at_sequence_start"}
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
@@ -38,10 +45,11 @@ def test_pins_catch_planted_mistake(name, tmp_path):
     (tmp_path / "oracle" / "oracle.c").write_text(src.replace(old, new, 1))
     (tmp_path / "tests").mkdir()
     shutil.copytree(os.path.join(ROOT, "tests", "golden"), tmp_path / "tests" / "golden")
-    for f in ("test_oracle.py", "conftest.py"):
+    suite = "test_oracle_multi.py" if name in MULTI else "test_oracle.py"
+    for f in (suite, "conftest.py"):
         shutil.copy(os.path.join(ROOT, "tests", f), tmp_path / "tests" / f)
     os.symlink(os.path.join(ROOT, "paper_2607_09207_amd"), tmp_path / "paper_2607_09207_amd")
     env = dict(os.environ, PYTHONPATH=str(tmp_path))
-    r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider", "tests/test_oracle.py"],
+    r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider", "tests/" + suite],
                        cwd=tmp_path, capture_output=True, text=True, env=env, timeout=300)
     assert r.returncode == 1 and "failed" in r.stdout, r.stdout[-2000:]
