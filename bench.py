@@ -49,7 +49,8 @@ def cpu_baseline(w, budget_s):
     }
 
 
-KERNEL_SOURCES = ["paper_2607_09207_amd/csrc/rlda_kernels.hip", "paper_2607_09207_amd/csrc/rlda_host.cpp",
+KERNEL_SOURCES = ["paper_2607_09207_amd/csrc/rlda_kernels.hip", "paper_2607_09207_amd/csrc/rlda_device.h",
+                  "paper_2607_09207_amd/csrc/rlda_host.cpp",
                   "paper_2607_09207_amd/csrc/rlda_params.h"]
 
 

@@ -139,6 +139,34 @@ class DecodeAttention:
             _abi.check(self._lib.rl_decode_attn_run_profiled(*args, e0, e1), "rl_decode_attn_run_profiled")
         return out
 
+    def multi(self, q, k_cache, v_cache, block_table, seq_lens, q_start, k_scale=None, v_scale=None, out=None,
+              workspace=None, stream=None, num_pages: Optional[int] = None, events=None):
+        """Multi-token queries (rl_decode_attn_run_multi): q [total_q][Hq][d], q_start
+        [batch + 1] int32 device tensor; sequence b's rows q[q_start[b]:q_start[b+1]]
+        are its last tokens and attend causally.  Returns out [total_q][Hq][d]."""
+        torch = _torch()
+        total = int(q.shape[0])
+        B = int(q_start.shape[0]) - 1
+        cfg = self.config
+        if out is None:
+            odt = torch.float32 if cfg.out_dtype == _abi.RLDA_F32 else torch.bfloat16
+            out = torch.empty((total, cfg.num_q_heads, cfg.head_dim), dtype=odt, device=q.device)
+        ws = workspace if workspace is not None else self.workspace(q.device)
+        if stream is None:
+            stream = torch.cuda.current_stream(q.device).cuda_stream
+        elif hasattr(stream, "cuda_stream"):
+            stream = stream.cuda_stream
+        npages = int(k_cache.shape[0]) if num_pages is None else int(num_pages)
+        ptr = lambda t: None if t is None else t.data_ptr()
+        wp = self._aligned_ptr(ws)
+        e0, e1 = (None, None) if events is None else tuple(self._event_handle(e) for e in events)
+        _abi.check(self._lib.rl_decode_attn_run_multi(self._h, B, npages, total, ptr(q), ptr(k_cache), ptr(v_cache),
+                                                      ptr(k_scale), ptr(v_scale), ptr(block_table), ptr(seq_lens),
+                                                      ptr(q_start), ptr(out), wp, ws.numel() - (wp - ws.data_ptr()),
+                                                      stream, e0, e1),
+                   "rl_decode_attn_run_multi")
+        return out
+
     def append(self, k_new, v_new, k_cache, v_cache, block_table, seq_lens, k_scale=None, v_scale=None,
                workspace=None, stream=None, num_pages: Optional[int] = None):
         """Write one decode step's K/V rows ([B][Hkv][d], the q dtype) into the caches at

@@ -13,7 +13,7 @@ STATUS = {0: "RLDA_OK", -1: "RLDA_ERR_INVALID_ARG", -2: "RLDA_ERR_UNSUPPORTED", 
 
 EXPORTS = ["rl_decode_attn_create", "rl_decode_attn_workspace_size", "rl_decode_attn_run",
            "rl_decode_attn_run_profiled", "rl_decode_attn_run_grouped", "rl_decode_attn_grouped_workspace_size",
-           "rl_decode_attn_append",
+           "rl_decode_attn_append", "rl_decode_attn_run_multi",
            "rl_decode_attn_read_flags", "rl_decode_attn_destroy", "rl_decode_attn_strerror"]
 
 
@@ -69,6 +69,8 @@ def load() -> ctypes.CDLL:
         lib.rl_decode_attn_grouped_workspace_size.restype = ctypes.c_int
         lib.rl_decode_attn_append.argtypes = [vp, i32, i32] + [vp] * 8 + [vp, sz, vp]
         lib.rl_decode_attn_append.restype = ctypes.c_int
+        lib.rl_decode_attn_run_multi.argtypes = [vp, i32, i32, i32] + [vp] * 9 + [vp, sz, vp, vp, vp]
+        lib.rl_decode_attn_run_multi.restype = ctypes.c_int
         lib.rl_decode_attn_read_flags.argtypes = [vp, vp, vp, ctypes.POINTER(ctypes.c_uint32)]
         lib.rl_decode_attn_read_flags.restype = ctypes.c_int
         lib.rl_decode_attn_destroy.argtypes = [vp]

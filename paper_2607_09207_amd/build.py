@@ -10,7 +10,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "librl_decode_attn.so")
-SOURCES = [os.path.join(CSRC, "rlda_kernels.hip"), os.path.join(CSRC, "rlda_host.cpp")]
+SOURCES = [os.path.join(CSRC, "rlda_kernels.hip"), os.path.join(CSRC, "rlda_multi.hip"),
+           os.path.join(CSRC, "rlda_host.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -38,10 +39,10 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
     return out
 
 
-def device_asm(out_path: str) -> str:
-    """Write the gfx950 assembly of the kernels (for register / spill review)."""
+def device_asm(out_path: str, source: int = 0) -> str:
+    """Write the gfx950 assembly of one kernel source (for register / spill review)."""
     cmd = [HIPCC] + [f for f in FLAGS if f not in ("-shared", "-fPIC")] + [
-        "--cuda-device-only", "-S", SOURCES[0], "-o", out_path]
+        "--cuda-device-only", "-S", SOURCES[source], "-o", out_path]
     subprocess.check_call(cmd, stderr=subprocess.DEVNULL)
     return out_path
 

@@ -335,6 +335,66 @@ rlda_status rl_decode_attn_append(rl_decode_attn_t h, int32_t batch, int32_t num
   return RLDA_OK;
 }
 
+rlda_status rl_decode_attn_run_multi(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32_t total_q,
+                                     const void* q, const void* k_cache, const void* v_cache, const float* k_scale,
+                                     const float* v_scale, const int32_t* block_table, const int32_t* seq_lens,
+                                     const int32_t* q_start, void* out, void* workspace, size_t workspace_bytes,
+                                     void* stream, void* event_begin, void* event_end) {
+  if (!h) return RLDA_ERR_INVALID_ARG;
+  const rl_decode_attn_config& c = h->cfg;
+  if (batch < 0 || batch > c.max_batch || num_pages < 0 || total_q < 0) return RLDA_ERR_INVALID_ARG;
+  if ((!event_begin) != (!event_end)) return RLDA_ERR_INVALID_ARG;
+  if (h->kind == rlda::KvKind::F32 || batch > rlda::kMultiMaxBatch) return RLDA_ERR_UNSUPPORTED;
+  // The kernel addresses q with 32-bit byte offsets.
+  if ((int64_t)total_q * c.num_q_heads * c.head_dim * 2 > INT32_MAX) return RLDA_ERR_UNSUPPORTED;
+  if (batch == 0 || total_q == 0) return RLDA_OK;
+  if (!q || !block_table || !seq_lens || !q_start || !out) return RLDA_ERR_INVALID_ARG;
+  if (num_pages > 0 && (!k_cache || !v_cache)) return RLDA_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out)) return RLDA_ERR_INVALID_ARG;
+  if (((uintptr_t)block_table & 3u) || ((uintptr_t)seq_lens & 3u) || ((uintptr_t)q_start & 3u))
+    return RLDA_ERR_INVALID_ARG;
+  if (h->kind == rlda::KvKind::FP8 && num_pages > 0 &&
+      (!k_scale || !v_scale || ((uintptr_t)k_scale & 3u) || ((uintptr_t)v_scale & 3u)))
+    return RLDA_ERR_INVALID_ARG;
+  const WsLayout wl = layout_of(h);
+  if (!workspace || ((uintptr_t)workspace % kAlign)) return RLDA_ERR_WORKSPACE;
+  if (workspace_bytes < wl.total) return RLDA_ERR_WORKSPACE;
+  // One workgroup per (128-row block, KV head): a sequence's n_b * G rows take at
+  // most n_b * G / 128 + 1 blocks, so this grid covers every consistent q_start.
+  const int64_t blocks = ((int64_t)total_q * h->group + rlda::kMultiRows - 1) / rlda::kMultiRows + batch;
+  const int64_t grid = blocks * c.num_kv_heads;
+  if (grid > INT32_MAX) return RLDA_ERR_UNSUPPORTED;
+  rlda::Params p;
+  memset(&p, 0, sizeof p);
+  p.q = q;
+  p.k = k_cache;
+  p.v = v_cache;
+  p.k_scale = k_scale;
+  p.v_scale = v_scale;
+  p.block_table = block_table;
+  p.seq_lens = seq_lens;
+  p.q_start = q_start;
+  p.total_q = total_q;
+  p.out = out;
+  p.flags = (uint32_t*)((char*)workspace + wl.flags);
+  const int eb = elem_bytes(c.kv_dtype);
+  p.stride_page = h->stride_page * eb;
+  p.stride_head = h->stride_head * eb;
+  p.stride_slot = (int32_t)(h->stride_slot * eb);
+  p.batch = batch;
+  p.num_pages = num_pages;
+  p.num_q_heads = c.num_q_heads;
+  p.num_kv_heads = c.num_kv_heads;
+  p.group = h->group;
+  p.max_pages = c.max_pages_per_seq;
+  p.scale_log2 = h->scale * 1.4426950408889634f;
+  p.out_bf16 = c.out_dtype == RLDA_BF16;
+  memcpy(p.q_head, h->q_head, sizeof p.q_head);
+  if (rlda::launch_multi(h->kind, c.head_dim, p, (int)grid, stream, event_begin, event_end) != hipSuccess)
+    return RLDA_ERR_HIP;
+  return RLDA_OK;
+}
+
 rlda_status rl_decode_attn_read_flags(rl_decode_attn_t h, const void* workspace, void* stream, uint32_t* flags) {
   if (!h || !workspace || !flags) return RLDA_ERR_INVALID_ARG;
   uint32_t v = 0;

@@ -42,17 +42,11 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "rlda_device.h"
 #include "rlda_params.h"
 
 namespace rlda {
 namespace {
-
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 #ifndef RLDA_MFMA_DEPTH
 #define RLDA_MFMA_DEPTH 3                    // pages in flight per wave, MFMA path
@@ -60,32 +54,7 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 #ifndef RLDA_MFMA_DEPTH_FP8
 #define RLDA_MFMA_DEPTH_FP8 RLDA_MFMA_DEPTH  // ... with fp8 pages (half the bytes each)
 #endif
-constexpr float kRescaleLog2 = 8.f;          // see Mfma::compute
 constexpr int kChunk = 64;                   // page ids fetched per vector load
-constexpr uint32_t kRsrcWord3 = 0x00020000u; // raw buffer, 32-bit data format
-constexpr int kLoadNT = 2;                   // cache policy: non-temporal (KV is read once)
-constexpr int kPastRange = 0x40000000;       // buffer offset beyond any descriptor's records: reads 0
-
-__device__ __forceinline__ float neg_inf() { return -__builtin_huge_valf(); }
-
-// Values equal in every lane, moved to scalar registers so that buffer
-// descriptors and loop bounds built from them stay scalar.
-__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
-__device__ __forceinline__ int64_t uni64(int64_t x) {
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)x);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)x >> 32));
-  return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, (int)kRsrcWord3);
-}
-
-// Descriptor from wave-uniform inputs, kept in scalar registers.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc_uni(const void* base, uint32_t bytes) {
-  const int64_t a = uni64((int64_t)(uintptr_t)base);
-  return make_rsrc((const void*)(uintptr_t)a, (uint32_t)uni((int)bytes));
-}
 
 template <int BYTES>
 struct RowLoad;
@@ -125,16 +94,6 @@ __device__ __forceinline__ float group_sum(float x) {
   return x + __shfl_xor(x, 32);
 }
 
-// Two OCP E4M3FN bytes of `w` (bytes 0,1 or, with hi_half, bytes 2,3) as floats.
-__device__ __forceinline__ f32x2 fp8x2_to_f32(uint32_t w, bool hi_half) {
-  return hi_half ? __builtin_amdgcn_cvt_pk_f32_fp8(w, true) : __builtin_amdgcn_cvt_pk_f32_fp8(w, false);
-}
-
-__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
-  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-  bf16x2 v = {(__bf16)lo, (__bf16)hi};
-  return __builtin_bit_cast(uint32_t, v);
-}
 
 
 // ---------------------------------------------------------------- helpers

@@ -1,0 +1,359 @@
+// Multi-token queries (prefill chunks) over the paged KV cache, for gfx950.
+//
+// Rollout runs prefill over the prompt tokens before it decodes them (Sec. 3,
+// rollout); the prefill cost model (App. A.1.2) charges its attention with a term
+// quadratic in the prompt length, so unlike decode this operation is a dense
+// contraction and runs on the matrix cores.  Sequence b brings n_b query rows (its
+// last n_b cached tokens, K/V already in the cache); row i attends causally to
+// positions 0 .. seq_lens[b] - n_b + i.
+//
+// Work.  The query rows of one (sequence, KV head) are its n_b * G (token, query
+// head) pairs, token-major, so every K/V row read serves all G heads sharing that
+// KV head.  A workgroup takes 128 of them: each of its 4 waves owns one 32-row
+// MFMA tile.  Workgroups are numbered so that each sequence's last row blocks,
+// which attend to the most keys, are dispatched first.
+//
+// Keys.  The workgroup walks its causal key range in blocks of 32 keys (two
+// pages).  Each wave stages one page of K or V of the next block into LDS (as
+// bf16; fp8 is converted exactly on the way) while the current block is computed:
+//   S^T[key][row] = K Q^T    v_mfma_f32_32x32x16_bf16, K from LDS, Q in registers;
+//   online softmax per row (lanes l and l^32 hold one row), with the reference
+//   maximum moved only when a score exceeds it by more than 2^8;
+//   O^T[d][row] += V^T P^T   the score registers are the P^T operand as they are;
+//                            V^T comes from the row-major V block through the
+//                            LDS transpose read (ds_read_b64_tr_b16).
+// The causal mask is evaluated only on blocks that reach a row's limit.  fp8 K
+// scales multiply the scores and V scales multiply P, per page.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "rlda_device.h"
+#include "rlda_params.h"
+
+namespace rlda {
+namespace {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+constexpr int kTile = 32;                     // query rows per wave = keys per block
+static_assert(kTile * kWaves == kMultiRows, "a workgroup's rows are its waves' tiles");
+
+template <int D, bool FP8>
+struct MqShape {
+  static constexpr int KS = D / 16;           // 32x32x16 k-steps of K Q^T
+  static constexpr int DT = D / 32;           // 32-wide output tiles of O^T
+  static constexpr int EB = FP8 ? 1 : 2;      // bytes per cached element
+  static constexpr int KRS = 2 * D + 16;      // LDS row stride of the K block (bytes, bf16 rows)
+  static constexpr int VRS = 2 * D + 32;      // ... of the V block (transpose reads conflict-free)
+  static constexpr int CPR = D * EB / 16;     // 16-byte chunks per cached row
+  static constexpr int LPL = kPage * CPR / 64; // 16-byte loads per lane to stage one page
+};
+
+// Exchange with the lane 32 away (the other half of a score row).
+__device__ __forceinline__ float swap32(float x) { return __shfl_xor(x, 32); }
+
+__device__ __forceinline__ bf16x4 lds_tr_read(const char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(__attribute__((address_space(3))) char*)p);
+}
+
+template <int D, bool FP8>
+__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(2, 2)))
+void multi_query_kernel(const Params p) {
+  using S = MqShape<D, FP8>;
+  __shared__ __align__(16) char s_k[2][kTile * S::KRS];
+  __shared__ __align__(16) char s_v[2][kTile * S::VRS];
+  __shared__ float s_scale[2][4];       // fp8: K scales of the block's pages 0, 1; then V's
+  __shared__ int32_t s_bad[2][2];       // page of the block not in the pool (contributes nothing)
+  __shared__ int32_t s_scan[kWaves];
+  __shared__ int16_t s_qh[kMaxQHeads];
+  extern __shared__ int32_t s_rb[];     // [batch + 1]: row blocks of the sequences before b
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
+  const int batch = p.batch, Hkv = p.num_kv_heads, G = p.group, Hq = p.num_q_heads;
+  const int cap = p.max_pages * kPage;
+
+  // 1. Row blocks per sequence and their prefix sums (identical in every workgroup).
+  //    A sequence whose offsets are inconsistent gets none and raises the flag.
+  {
+    const int per = (batch + kThreads - 1) / kThreads;
+    const int lo = min(tid * per, batch), hi = min(lo + per, batch);
+    int sum = 0, bad = 0;
+    for (int b = lo; b < hi; ++b) {
+      const int q0 = p.q_start[b], q1 = p.q_start[b + 1];
+      const bool ok = q0 >= 0 && q1 >= q0 && q1 <= p.total_q;
+      bad |= !ok;
+      const int nrb = ok ? (int)(((int64_t)(q1 - q0) * G + kMultiRows - 1) / kMultiRows) : 0;
+      s_rb[b + 1] = nrb;
+      sum += nrb;
+    }
+    if (bad && blockIdx.x == 0) atomicOr(p.flags, kFlagBadLen);
+    int x = sum;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) s_scan[wave] = x;
+    for (int e = tid; e < Hq; e += kThreads) s_qh[e] = p.q_head[e];
+    __syncthreads();
+    int run = x - sum;
+    for (int w = 0; w < wave; ++w) run += s_scan[w];
+    for (int b = lo; b < hi; ++b) {
+      run += s_rb[b + 1];
+      s_rb[b + 1] = run;
+    }
+    if (tid == 0) s_rb[0] = 0;
+    __syncthreads();
+  }
+  const int64_t items = (int64_t)s_rb[batch] * Hkv;
+  if (blockIdx.x == 0 && tid == 0 && items > (int64_t)gridDim.x) atomicOr(p.flags, kFlagBadLen);
+  const int u = blockIdx.x;
+  if (u >= items) return;
+
+  // 2. This workgroup's (sequence b, row block rb, KV head g).
+  const int g = u % Hkv, rbg = u / Hkv;
+  int b = 0;
+  {
+    int lo = 0, hi = batch;   // s_rb[lo] <= rbg < s_rb[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (s_rb[mid] <= rbg) lo = mid; else hi = mid;
+    }
+    b = uni(lo);
+  }
+  const int rb = s_rb[b + 1] - 1 - rbg;               // the sequence's last row block first
+  const int q0 = p.q_start[b], n = p.q_start[b + 1] - q0;
+  int L = p.seq_lens[b];
+  if (L < 0 || L > cap || n > L) {
+    if (tid == 0) atomicOr(p.flags, kFlagBadLen);
+    L = min(max(L, 0), cap);
+  }
+  const int rows = n * G;
+  const int r0 = rb * kMultiRows, r1 = min(r0 + kMultiRows, rows);
+  const int base_pos = L - n;                                   // position of query token 0
+  const int E = max(0, base_pos + (r1 - 1) / G + 1);            // keys the workgroup reads
+  const int nkb = (E + kTile - 1) / kTile;
+  const int wr0 = r0 + kTile * wave, wr1 = min(wr0 + kTile, r1);
+  const int Ew = wr0 < wr1 ? max(0, base_pos + (wr1 - 1) / G + 1) : 0;       // keys this wave needs
+  const int Ew_full = wr0 < wr1 ? max(0, base_pos + wr0 / G + 1) : 0;       // ... visible to all its rows
+
+  // This lane's query row: lanes i and i + 32 share row wr0 + i.
+  const int i = lane & 31, hh = lane >> 5;
+  const int row = wr0 + i;
+  const bool live = row < wr1;
+  const int qi = live ? row / G : 0;
+  const int head = live ? s_qh[g * G + (row - qi * G)] : 0;
+  const int lim = live ? base_pos + qi + 1 : 0;                 // keys [0, lim) are visible
+
+  // Q operand (B of K Q^T): lane 32h + i holds row i's elements [16s + 8h, 16s + 8h + 8).
+  bf16x8 qop[S::KS];
+  {
+    const __amdgpu_buffer_rsrc_t rq = make_rsrc_uni(p.q, (uint32_t)p.total_q * (uint32_t)Hq * D * 2u);
+    const int off = live ? ((q0 + qi) * Hq + head) * D * 2 : kPastRange;
+#pragma unroll
+    for (int s = 0; s < S::KS; ++s)
+      qop[s] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rq, off + 16 * (2 * s + hh), 0, 0));
+  }
+
+  // Staging: wave w brings page (w & 1) of each block's K (w < 2) or V (w >= 2).
+  const int which = wave >> 1, pgw = wave & 1;
+  const char* pool = (const char*)(which ? p.v : p.k);
+  const float* scl = which ? p.v_scale : p.k_scale;
+  u32x4 stg[S::LPL];
+  float stg_scale = 0.f;
+  int stg_bad = 0;
+  auto stage_load = [&](int kb) {
+    const int j = 2 * kb + pgw;   // page index in the sequence
+    int tok = min(max(E - j * kPage, 0), kPage);
+    int pid = 0;
+    stg_bad = 0;
+    if (tok > 0) {
+      pid = uni(p.block_table[(int64_t)b * p.max_pages + j]);
+      if ((unsigned)pid >= (unsigned)p.num_pages) {
+        if (lane == 0) atomicOr(p.flags, kFlagBadPage);
+        tok = 0;
+        stg_bad = 1;
+      }
+    }
+    const int64_t po = tok > 0 ? (int64_t)pid * p.stride_page + (int64_t)g * p.stride_head : 0;
+    const uint32_t nrec = tok > 0 ? (uint32_t)((tok - 1) * p.stride_slot + D * S::EB) : 0u;
+    const __amdgpu_buffer_rsrc_t r = make_rsrc_uni(pool + po, nrec);
+#pragma unroll
+    for (int k = 0; k < S::LPL; ++k) {
+      const int ci = lane + 64 * k, rr = ci / S::CPR, c = ci % S::CPR;
+      stg[k] = __builtin_amdgcn_raw_buffer_load_b128(r, rr * p.stride_slot + 16 * c, 0, 0);
+    }
+    if constexpr (FP8) stg_scale = tok > 0 ? scl[(int64_t)pid * Hkv + g] : 0.f;
+  };
+  auto stage_write = [&](int buf) {
+    char* dst = which ? s_v[buf] : s_k[buf];
+    const int RS = which ? S::VRS : S::KRS;
+#pragma unroll
+    for (int k = 0; k < S::LPL; ++k) {
+      const int ci = lane + 64 * k, rr = ci / S::CPR, c = ci % S::CPR;
+      char* rowp = dst + (kPage * pgw + rr) * RS;
+      if constexpr (!FP8) {
+        *(u32x4*)(rowp + 16 * c) = stg[k];
+      } else {   // 16 E4M3 values -> 16 bf16 (exact)
+        uint32_t w[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const f32x2 a = fp8x2_to_f32(stg[k][e], false), bb = fp8x2_to_f32(stg[k][e], true);
+          w[2 * e] = pack_bf16(a[0], a[1]);
+          w[2 * e + 1] = pack_bf16(bb[0], bb[1]);
+        }
+        *(u32x4*)(rowp + 32 * c) = u32x4{w[0], w[1], w[2], w[3]};
+        *(u32x4*)(rowp + 32 * c + 16) = u32x4{w[4], w[5], w[6], w[7]};
+      }
+    }
+    if (lane == 0) {
+      if constexpr (FP8) s_scale[buf][2 * which + pgw] = stg_scale;
+      if (which == 0) s_bad[buf][pgw] = stg_bad;
+    }
+  };
+
+  f32x16 acc[S::DT];
+#pragma unroll
+  for (int t = 0; t < S::DT; ++t) acc[t] = f32x16{};
+  float m = neg_inf(), l = 0.f;
+
+  auto compute = [&](int kb, int buf) {
+    const char* kl = s_k[buf];
+    const char* vl = s_v[buf];
+    f32x16 sc = f32x16{};
+#pragma unroll
+    for (int s = 0; s < S::KS; ++s) {
+      const bf16x8 a = *(const bf16x8*)(kl + i * S::KRS + 16 * (2 * s + hh));
+      sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qop[s], sc, 0, 0, 0);
+    }
+    // Lane 32h + i holds S^T[key 8(j/4) + 4h + j%4][row i], j < 16: page 0 for j < 8.
+    float km0 = p.scale_log2, km1 = p.scale_log2, vm0 = 1.f, vm1 = 1.f;
+    if constexpr (FP8) {
+      km0 *= s_scale[buf][0];
+      km1 *= s_scale[buf][1];
+      vm0 = s_scale[buf][2];
+      vm1 = s_scale[buf][3];
+    }
+    const int bad0 = s_bad[buf][0], bad1 = s_bad[buf][1];
+    float sv[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) sv[j] = sc[j] * (j < 8 ? km0 : km1);
+    if ((kb + 1) * kTile > Ew_full || bad0 || bad1) {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const int key = kb * kTile + 8 * (j >> 2) + 4 * hh + (j & 3);
+        if (key >= lim || (j < 8 ? bad0 : bad1)) sv[j] = neg_inf();
+      }
+    }
+    float mx = sv[0];
+#pragma unroll
+    for (int j = 1; j < 16; ++j) mx = fmaxf(mx, sv[j]);
+    mx = fmaxf(mx, swap32(mx));
+    // Lazy rescale: the reference maximum moves only when a score exceeds it by
+    // more than 2^kRescaleLog2 (always when it is still -inf and a score is not).
+    // A row whose keys are all masked so far keeps m = -inf and alpha = 1.
+    const bool up = mx > m + kRescaleLog2;
+    if (__builtin_amdgcn_ballot_w64(up) != 0) {
+      const float alpha = up ? __builtin_amdgcn_exp2f(m - mx) : 1.f;
+      l *= alpha;
+      m = up ? mx : m;
+#pragma unroll
+      for (int t = 0; t < S::DT; ++t) acc[t] *= alpha;
+    }
+    const float mu = (m == neg_inf()) ? 0.f : m;
+    float pr[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      pr[j] = __builtin_amdgcn_exp2f(sv[j] - mu);
+      l += pr[j];
+    }
+    // P^T operand of key step kk: K position 8h + e is key 16kk + 8(e/4) + 4h + e%4.
+    bf16x8 pb[2];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const float vm = kk ? vm1 : vm0;
+      const u32x4 w = {pack_bf16(pr[8 * kk] * vm, pr[8 * kk + 1] * vm), pack_bf16(pr[8 * kk + 2] * vm, pr[8 * kk + 3] * vm),
+                       pack_bf16(pr[8 * kk + 4] * vm, pr[8 * kk + 5] * vm), pack_bf16(pr[8 * kk + 6] * vm, pr[8 * kk + 7] * vm)};
+      pb[kk] = __builtin_bit_cast(bf16x8, w);
+    }
+    // V^T operand: the transpose read gives lane (16-lane group q, index c) the 4
+    // keys k0 .. k0+3 of column d = 16 (q & 1) + c of the tile, when lane c' of
+    // the group addresses key k0 + c'/4, columns 4 (c' % 4) .. +3.
+    const int lr = (lane & 15) >> 2, lc = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const char* vr = vl + (16 * kk + 4 * hh + lr) * S::VRS;
+#pragma unroll
+      for (int t = 0; t < S::DT; ++t) {
+        const bf16x4 x0 = lds_tr_read(vr + 2 * (32 * t + lc));
+        const bf16x4 x1 = lds_tr_read(vr + 8 * S::VRS + 2 * (32 * t + lc));
+        const bf16x8 a = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+        acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kk], acc[t], 0, 0, 0);
+      }
+    }
+  };
+
+  // 3. Key blocks: stage block kb + 1 while block kb is computed.
+  if (nkb > 0) {
+    stage_load(0);
+    stage_write(0);
+  }
+  __syncthreads();
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int buf = kb & 1;
+    if (kb + 1 < nkb) stage_load(kb + 1);
+    if (kb * kTile < Ew) compute(kb, buf);
+    if (kb + 1 < nkb) stage_write(buf ^ 1);
+    __syncthreads();
+  }
+
+  // 4. Normalise and write: lane 32h + i holds O^T[d = 32t + 8jj + 4h + 0..3][row i].
+  const float lt = l + swap32(l);
+  if (!live) return;
+  const float inv = lt > 0.f ? 1.f / lt : 0.f;
+  const int64_t ob = ((int64_t)(q0 + qi) * Hq + head) * D;
+#pragma unroll
+  for (int t = 0; t < S::DT; ++t)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const int d = 32 * t + 8 * jj + 4 * hh;
+      const float o0 = acc[t][4 * jj] * inv, o1 = acc[t][4 * jj + 1] * inv;
+      const float o2 = acc[t][4 * jj + 2] * inv, o3 = acc[t][4 * jj + 3] * inv;
+      if (p.out_bf16)
+        *(u32x2*)((uint16_t*)p.out + ob + d) = u32x2{pack_bf16(o0, o1), pack_bf16(o2, o3)};
+      else
+        *(f32x4*)((float*)p.out + ob + d) = f32x4{o0, o1, o2, o3};
+    }
+}
+
+template <int D, bool FP8>
+int launch_multi_t(const Params& p, int grid, void* stream, void* ev_begin, void* ev_end) {
+  hipStream_t st = (hipStream_t)stream;
+  if (ev_begin && hipEventRecord((hipEvent_t)ev_begin, st) != hipSuccess) return -1;
+  const size_t lds = sizeof(int32_t) * ((size_t)p.batch + 1);
+  hipLaunchKernelGGL((multi_query_kernel<D, FP8>), dim3(grid), dim3(kThreads), lds, st, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return (int)e;
+  if (ev_end && hipEventRecord((hipEvent_t)ev_end, st) != hipSuccess) return -1;
+  return 0;
+}
+
+}  // namespace
+
+int launch_multi(KvKind kind, int head_dim, const Params& p, int grid, void* stream, void* ev_begin, void* ev_end) {
+  switch (kind) {
+    case KvKind::BF16:
+      return head_dim == 128 ? launch_multi_t<128, false>(p, grid, stream, ev_begin, ev_end)
+                             : launch_multi_t<64, false>(p, grid, stream, ev_begin, ev_end);
+    case KvKind::FP8:
+      return head_dim == 128 ? launch_multi_t<128, true>(p, grid, stream, ev_begin, ev_end)
+                             : launch_multi_t<64, true>(p, grid, stream, ev_begin, ev_end);
+    case KvKind::F32:
+      break;
+  }
+  return -1;
+}
+
+}  // namespace rlda

@@ -55,6 +55,9 @@ struct Params {
   // KV append (rl_decode_attn_append): the step's new rows, [batch][Hkv][D] in the q dtype.
   const void* k_in;
   const void* v_in;
+  // Multi-token queries (rl_decode_attn_run_multi): q and out are [total_q][Hq][D].
+  const int32_t* q_start;      // [batch + 1] query-row offsets
+  int32_t total_q;
   int16_t q_head[kMaxQHeads];  // q_head[g * G + i] = i-th query head of KV head g
 };
 
@@ -70,5 +73,9 @@ int launch_grouped(KvKind kind, int head_dim, int group, const Params& p, int ng
                    void* ev_begin, void* ev_end);
 // KV append: one wave per (sequence, KV head).
 int launch_append(KvKind kind, int head_dim, const Params& p, void* stream);
+// Multi-token queries (rlda_multi.hip): one workgroup per (128-row query block, KV head).
+int launch_multi(KvKind kind, int head_dim, const Params& p, int grid, void* stream, void* ev_begin, void* ev_end);
+constexpr int kMultiRows = 128;    // query rows (token, head pairs) per workgroup of the multi-token kernel
+constexpr int kMultiMaxBatch = 4096;   // its per-sequence LDS table stays within 64 KiB of LDS per workgroup
 
 }  // namespace rlda

@@ -207,3 +207,35 @@ def test_append_rejects_bad_arguments_before_launch(lib):
     assert app(batch=0) == 0
     assert lib.rl_decode_attn_append(None, 1, 1, *([f] * 8), f, 1, None) == -1
     lib.rl_decode_attn_destroy(h)
+
+
+def test_multi_rejects_bad_arguments_before_launch(lib):
+    st, h = create(lib, cfg(kv_dtype=_abi.RLDA_FP8_E4M3FN, max_batch=8192, max_pages_per_seq=64))
+    assert st == 0
+    n = ctypes.c_size_t()
+    lib.rl_decode_attn_workspace_size(h, ctypes.byref(n))
+    f = 0x10000
+
+    def multi(batch=4, total=100, q=f, ks=f, qs=f, out=f, ws=f * 16, wsb=None, e0=None, e1=None, handle=h):
+        return lib.rl_decode_attn_run_multi(handle, batch, 10, total, q, f, f, ks, f, f, f, qs, out, ws,
+                                            n.value if wsb is None else wsb, None, e0, e1)
+
+    assert multi(q=None) == -1
+    assert multi(q=f + 8) == -1           # misaligned
+    assert multi(qs=None) == -1           # q_start required
+    assert multi(qs=f + 2) == -1
+    assert multi(out=None) == -1
+    assert multi(ks=None) == -1           # fp8 needs scales
+    assert multi(total=-1) == -1
+    assert multi(e0=f) == -1              # events: both or neither
+    assert multi(ws=None) == -4
+    assert multi(wsb=n.value - 1) == -4
+    assert multi(batch=4097) == -2        # beyond the multi-token kernel's batch limit
+    assert multi(total=(1 << 31) // (28 * 128 * 2) + 1) == -2   # q beyond 2^31 bytes
+    assert multi(batch=0) == 0 and multi(total=0) == 0
+    lib.rl_decode_attn_destroy(h)
+    st, h32 = create(lib, cfg(num_q_heads=4, num_kv_heads=4, head_dim=64, q_dtype=0, kv_dtype=0, out_dtype=0,
+                              max_pages_per_seq=16))
+    assert st == 0
+    assert multi(handle=h32) == -2        # fp32 caches: no multi-token path
+    lib.rl_decode_attn_destroy(h32)
