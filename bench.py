@@ -18,6 +18,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0   # MI355X HBM3E
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 
 
 def log(msg):
@@ -54,18 +55,22 @@ KERNEL_SOURCES = ["paper_2607_09207_amd/csrc/rlda_kernels.hip", "paper_2607_0920
                   "paper_2607_09207_amd/csrc/rlda_params.h"]
 
 
-def kernel_source_hash():
+MULTI_SOURCES = ["paper_2607_09207_amd/csrc/rlda_multi.hip", "paper_2607_09207_amd/csrc/rlda_device.h",
+                 "paper_2607_09207_amd/csrc/rlda_host.cpp", "paper_2607_09207_amd/csrc/rlda_params.h"]
+
+
+def kernel_source_hash(sources=None):
     import hashlib
     hsh = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in sources or KERNEL_SOURCES:
         hsh.update(open(os.path.join(ROOT, f), "rb").read())
     return hsh.hexdigest()[:16]
 
 
-def measured_traffic(workload):
+def measured_traffic(workload, sources=None):
     """HBM bytes per launch from the committed counter summary of this workload
     (FETCH_SIZE and WRITE_SIZE scaled by the copy-kernel factors), or None when
-    there is none or the kernel sources changed since it was taken."""
+    there is none or the kernel's sources changed since it was taken."""
     path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.md")
     if not os.path.exists(path):
         return None
@@ -74,7 +79,7 @@ def measured_traffic(workload):
         if ln.startswith("- ") and ":" in ln:
             k, v = ln[2:].split(":", 1)
             fields[k.strip()] = v.strip().strip("`")
-    if fields.get("kernel_source_hash") != kernel_source_hash():
+    if fields.get("kernel_source_hash") != kernel_source_hash(sources):
         return None
     try:
         return int(fields["traffic_bytes_per_launch"])
@@ -154,6 +159,98 @@ def append_bench(args, torch, dev, w, h, ws):
     }), flush=True)
 
 
+def multi_bench(args, torch, dev, w, h, ws):
+    """Time multi-token (prefill chunk) attention, rl_decode_attn_run_multi.  One step
+    = one call over the workload's query rows; the metric is algorithmic TFLOP/s
+    (4 d flops per visible (row, key) pair and query head, causal)."""
+    import numpy as np
+    import oracle
+    from paper_2607_09207_amd import accounting as A
+    from paper_2607_09207_amd import inputs as I
+    sets = [I.to_torch(w, dev)]
+    for _ in range(args.sets - 1):
+        s = dict(sets[0])
+        s["k_cache"] = sets[0]["k_cache"].clone()
+        s["v_cache"] = sets[0]["v_cache"].clone()
+        sets.append(s)
+    qs = torch.from_numpy(np.ascontiguousarray(w.q_start, np.int32)).to(dev)
+    rows = int(w.q_start[-1])
+    out = torch.empty((rows, w.num_q_heads, w.head_dim), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def call(i, events=None):
+        s = sets[i % len(sets)]
+        h.multi(s["q"], s["k_cache"], s["v_cache"], s["block_table"], s["seq_lens"], qs, k_scale=s["k_scale"],
+                v_scale=s["v_scale"], out=out, workspace=ws, stream=stream, events=events)
+
+    log(f"warmup {args.warmup}")
+    for i in range(args.warmup):
+        call(i)
+    torch.cuda.synchronize()
+    log(f"timing {args.steps} steps")
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(args.steps):
+        call(i)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t0.elapsed_time(t1) / args.steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a, b in ev:
+        a.record(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        call(i, events=ev[i])
+    torch.cuda.synchronize()
+    per_call = np.array([a.elapsed_time(b) for a, b in ev])
+    kern_ms = float(per_call.mean())
+    flops, nbytes = A.multi_flops(w), A.multi_bytes(w)
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    t_mfma, t_hbm = flops / (PEAK_BF16_TFLOPS * 1e12), nbytes / (PEAK_HBM_GBS * 1e9)
+    if t_mfma >= t_hbm:
+        roof = {"bound": "mfma", "achieved": round(flops / (kern_ms * 1e-3) / 1e12, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": round(nbytes / (kern_ms * 1e-3) / 1e9, 2), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s"}
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = measured_traffic(w.name, MULTI_SOURCES)
+    log(f"ms/step {ms_per_step:.4f}  kernel avg {kern_ms:.4f} ms (p10 {np.percentile(per_call, 10):.4f}, "
+        f"p90 {np.percentile(per_call, 90):.4f})  {value:.1f} TFLOP/s  rows/s {rows / (ms_per_step * 1e-3):.0f}")
+    result = {
+        "metric": "multi-token (prefill chunk) attention TFLOP/s at 1 GPU", "value": round(value, 3),
+        "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if w.kv_dtype == "bf16" else "fp8", "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "query_rows": rows, "num_q_heads": w.num_q_heads,
+                   "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "kv_dtype": w.kv_dtype,
+                   "sum_seq_lens": int(w.seq_lens.sum()), "flops_per_step": flops, "bytes_per_step": nbytes,
+                   "query_rows_per_s": round(rows / (ms_per_step * 1e-3), 1), "kv_sets_rotated": len(sets)},
+        "roofline": roof,
+    }
+    if args.cpu_budget > 0:
+        # the oracle on whole sequences, shortest first, until the budget is spent
+        log("cpu baseline (oracle)")
+        order = np.argsort(np.diff(np.asarray(w.q_start)) * w.seq_lens)
+        done_flops, el, picked = 0, 0.0, 0
+        for b in order:
+            mask = np.zeros(w.batch, np.uint8)
+            mask[b] = 1
+            t_s = time.perf_counter()
+            oracle.run_multi(w, batch_mask=mask)
+            el += time.perf_counter() - t_s
+            wb = I.with_query_rows(w, [int(w.q_start[b + 1] - w.q_start[b]) if j == b else 0 for j in range(w.batch)])
+            done_flops += A.multi_flops(wb)
+            picked += 1
+            if el >= args.cpu_budget:
+                break
+        result["cpu_baseline"] = {"value": round(done_flops / el / 1e12, 6), "unit": "TFLOP/s",
+                                  "cores": oracle.max_threads(), "kind": "oracle",
+                                  "sample": f"the {picked} cheapest sequences of {w.name}, whole, fp64, {el:.1f} s wall"}
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -163,8 +260,10 @@ def main():
     ap.add_argument("--sets", type=int, default=3, help="KV pool copies rotated across calls")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of CPU oracle work (0 = skip)")
     ap.add_argument("--ranges", type=int, default=0, help="force the number of work ranges (tuning)")
-    ap.add_argument("--mode", choices=["attention", "append", "copy"], default="attention",
+    ap.add_argument("--mode", choices=["attention", "append", "multi", "copy"], default="attention",
                     help="append: the per-step KV append (rl_decode_attn_append) on the workload's last tokens; "
+                         "multi: multi-token (prefill chunk) attention on a multi-token workload "
+                         "(prompt_prefill_grpo_bf16, chunked_prefill_gqa_bf16); "
                          "copy: a plain device copy of --copy-mib MiB, the reference for HBM counter scaling")
     ap.add_argument("--copy-mib", type=int, default=256)
     ap.add_argument("--prompt-tokens", type=int, default=0,
@@ -205,6 +304,10 @@ def main():
                         num_work_ranges=args.ranges)
     if args.mode == "append":
         return append_bench(args, torch, dev, w, h, h.workspace(dev))
+    if (args.mode == "multi") != (w.q_start is not None):
+        raise SystemExit("--mode multi goes with the multi-token workloads: " + ", ".join(I.MULTI_WORKLOADS))
+    if args.mode == "multi":
+        return multi_bench(args, torch, dev, w, h, h.workspace(dev))
     sets = [I.to_torch(w, dev)]
     for _ in range(args.sets - 1):
         s = dict(sets[0])

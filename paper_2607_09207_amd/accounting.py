@@ -64,3 +64,33 @@ def call_bytes(w) -> dict:
 def algorithmic_bytes(w) -> int:
     c = call_bytes(w)
     return c["kv_unique"] + c["scales"] + c["q"] + c["out"] + c["block_table"] + c["seq_lens"]
+
+
+# ------------------------------------------------------------------ multi-token queries
+
+def causal_pairs(w) -> int:
+    """(query row, visible key) pairs per query head of a multi-token call: row i of
+    the n_b rows of sequence b sees seq_lens[b] - n_b + i + 1 keys, so the sum is
+    n_b (L_b - n_b) + n_b (n_b + 1) / 2."""
+    L = np.asarray(w.seq_lens, np.int64)
+    n = np.diff(np.asarray(w.q_start, np.int64))
+    return int(np.sum(n * (L - n) + n * (n + 1) // 2))
+
+
+def multi_flops(w) -> int:
+    """Algorithmic flops of one multi-token call: q.k and p.v, 2 * d each, per visible
+    (row, key) pair and query head.  This is the causal count; the prefill term of
+    App. A.1.2 (4 L H p^2 per sequence) counts the full p x p square, twice this for
+    a whole prompt."""
+    return 4 * w.head_dim * w.num_q_heads * causal_pairs(w)
+
+
+def multi_bytes(w) -> int:
+    """Algorithmic bytes of one multi-token call: every cached token's K and V once,
+    fp8 scales, q rows, fp32 output rows, block-table entries, offsets and lengths."""
+    bpt = b_kv(1, w.num_kv_heads, w.head_dim, DTYPE_BYTES[w.kv_dtype])
+    rows = int(w.q_start[-1])
+    pages = int(np.sum(w.pages_used()))
+    scales = 8 * w.num_kv_heads * pages if w.kv_dtype == "fp8_e4m3fn" else 0
+    return int(bpt * int(np.sum(w.seq_lens.astype(np.int64)))) + scales + rows * w.num_q_heads * w.head_dim * (
+        DTYPE_BYTES[w.q_dtype] + 4) + 4 * pages + 8 * w.batch + 4

@@ -14,8 +14,10 @@
 // which attend to the most keys, are dispatched first.
 //
 // Keys.  The workgroup walks its causal key range in blocks of 32 keys (two
-// pages).  Each wave stages one page of K or V of the next block into LDS (as
-// bf16; fp8 is converted exactly on the way) while the current block is computed:
+// pages).  Each wave loads one page of K or V of a block into registers two
+// blocks ahead (page ids come through the scalar cache one block before that) and
+// writes it to LDS (as bf16; fp8 is converted exactly on the way) while the block
+// before it is computed:
 //   S^T[key][row] = K Q^T    v_mfma_f32_32x32x16_bf16, K from LDS, Q in registers;
 //   online softmax per row (lanes l and l^32 hold one row), with the reference
 //   maximum moved only when a score exceeds it by more than 2^8;
@@ -37,7 +39,17 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
+#ifndef RLDA_MQ_KPAD
+#define RLDA_MQ_KPAD 16                       // LDS row padding of the K block (bytes)
+#endif
+#ifndef RLDA_MQ_VPAD
+#define RLDA_MQ_VPAD 32                       // ... of the V block
+#endif
 constexpr int kTile = 32;                     // query rows per wave = keys per block
+constexpr int kBufs = 2;                      // LDS block buffers
+#ifndef RLDA_MQ_PREFETCH
+#define RLDA_MQ_PREFETCH 2                    // blocks loaded ahead into registers
+#endif
 static_assert(kTile * kWaves == kMultiRows, "a workgroup's rows are its waves' tiles");
 
 template <int D, bool FP8>
@@ -45,8 +57,8 @@ struct MqShape {
   static constexpr int KS = D / 16;           // 32x32x16 k-steps of K Q^T
   static constexpr int DT = D / 32;           // 32-wide output tiles of O^T
   static constexpr int EB = FP8 ? 1 : 2;      // bytes per cached element
-  static constexpr int KRS = 2 * D + 16;      // LDS row stride of the K block (bytes, bf16 rows)
-  static constexpr int VRS = 2 * D + 32;      // ... of the V block (transpose reads conflict-free)
+  static constexpr int KRS = 2 * D + RLDA_MQ_KPAD;   // LDS row stride of the K block (bytes, bf16 rows)
+  static constexpr int VRS = 2 * D + RLDA_MQ_VPAD;   // ... of the V block
   static constexpr int CPR = D * EB / 16;     // 16-byte chunks per cached row
   static constexpr int LPL = kPage * CPR / 64; // 16-byte loads per lane to stage one page
 };
@@ -62,10 +74,12 @@ template <int D, bool FP8>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(2, 2)))
 void multi_query_kernel(const Params p) {
   using S = MqShape<D, FP8>;
-  __shared__ __align__(16) char s_k[2][kTile * S::KRS];
-  __shared__ __align__(16) char s_v[2][kTile * S::VRS];
-  __shared__ float s_scale[2][4];       // fp8: K scales of the block's pages 0, 1; then V's
-  __shared__ int32_t s_bad[2][2];       // page of the block not in the pool (contributes nothing)
+  // Two block buffers: block kb is computed from one while block kb + 1 is written
+  // to the other.
+  __shared__ __align__(16) char s_k[kBufs][kTile * S::KRS];
+  __shared__ __align__(16) char s_v[kBufs][kTile * S::VRS];
+  __shared__ float s_scale[kBufs][4];   // fp8: K scales of the block's pages 0, 1; then V's
+  __shared__ int32_t s_bad[kBufs][2];   // page of the block not in the pool (contributes nothing)
   __shared__ int32_t s_scan[kWaves];
   __shared__ int16_t s_qh[kMaxQHeads];
   extern __shared__ int32_t s_rb[];     // [batch + 1]: row blocks of the sequences before b
@@ -161,20 +175,27 @@ void multi_query_kernel(const Params p) {
   const int which = wave >> 1, pgw = wave & 1;
   const char* pool = (const char*)(which ? p.v : p.k);
   const float* scl = which ? p.v_scale : p.k_scale;
-  u32x4 stg[S::LPL];
-  float stg_scale = 0.f;
-  int stg_bad = 0;
-  auto stage_load = [&](int kb) {
+  // Register sets of the blocks in flight: block kb is loaded into set kb % PD
+  // PD blocks before it is computed (global latency is several blocks' work).
+  constexpr int PD = RLDA_MQ_PREFETCH;
+  u32x4 stg[PD][S::LPL];
+  float stg_scale[PD];
+  int stg_bad[PD];
+  // Page ids come through the scalar cache (the block table is read-only here),
+  // one block ahead of the loads that use them; the index is clamped into the row
+  // so the load is always in bounds (pages past the keys are not used).
+  typedef const __attribute__((address_space(4))) int32_t bt_elem;
+  bt_elem* bt_row = (bt_elem*)(const void*)(p.block_table + (int64_t)b * p.max_pages);
+  auto page_id = [&](int kb) { return bt_row[min(2 * kb + pgw, p.max_pages - 1)]; };
+  auto stage_load = [&](int kb, int set, int pid) {
     const int j = 2 * kb + pgw;   // page index in the sequence
     int tok = min(max(E - j * kPage, 0), kPage);
-    int pid = 0;
-    stg_bad = 0;
+    stg_bad[set] = 0;
     if (tok > 0) {
-      pid = uni(p.block_table[(int64_t)b * p.max_pages + j]);
       if ((unsigned)pid >= (unsigned)p.num_pages) {
         if (lane == 0) atomicOr(p.flags, kFlagBadPage);
         tok = 0;
-        stg_bad = 1;
+        stg_bad[set] = 1;
       }
     }
     const int64_t po = tok > 0 ? (int64_t)pid * p.stride_page + (int64_t)g * p.stride_head : 0;
@@ -183,11 +204,11 @@ void multi_query_kernel(const Params p) {
 #pragma unroll
     for (int k = 0; k < S::LPL; ++k) {
       const int ci = lane + 64 * k, rr = ci / S::CPR, c = ci % S::CPR;
-      stg[k] = __builtin_amdgcn_raw_buffer_load_b128(r, rr * p.stride_slot + 16 * c, 0, 0);
+      stg[set][k] = __builtin_amdgcn_raw_buffer_load_b128(r, rr * p.stride_slot + 16 * c, 0, 0);
     }
-    if constexpr (FP8) stg_scale = tok > 0 ? scl[(int64_t)pid * Hkv + g] : 0.f;
+    if constexpr (FP8) stg_scale[set] = tok > 0 ? scl[(int64_t)pid * Hkv + g] : 0.f;
   };
-  auto stage_write = [&](int buf) {
+  auto stage_write = [&](int set, int buf) {
     char* dst = which ? s_v[buf] : s_k[buf];
     const int RS = which ? S::VRS : S::KRS;
 #pragma unroll
@@ -195,12 +216,12 @@ void multi_query_kernel(const Params p) {
       const int ci = lane + 64 * k, rr = ci / S::CPR, c = ci % S::CPR;
       char* rowp = dst + (kPage * pgw + rr) * RS;
       if constexpr (!FP8) {
-        *(u32x4*)(rowp + 16 * c) = stg[k];
+        *(u32x4*)(rowp + 16 * c) = stg[set][k];
       } else {   // 16 E4M3 values -> 16 bf16 (exact)
         uint32_t w[8];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const f32x2 a = fp8x2_to_f32(stg[k][e], false), bb = fp8x2_to_f32(stg[k][e], true);
+          const f32x2 a = fp8x2_to_f32(stg[set][k][e], false), bb = fp8x2_to_f32(stg[set][k][e], true);
           w[2 * e] = pack_bf16(a[0], a[1]);
           w[2 * e + 1] = pack_bf16(bb[0], bb[1]);
         }
@@ -209,8 +230,8 @@ void multi_query_kernel(const Params p) {
       }
     }
     if (lane == 0) {
-      if constexpr (FP8) s_scale[buf][2 * which + pgw] = stg_scale;
-      if (which == 0) s_bad[buf][pgw] = stg_bad;
+      if constexpr (FP8) s_scale[buf][2 * which + pgw] = stg_scale[set];
+      if (which == 0) s_bad[buf][pgw] = stg_bad[set];
     }
   };
 
@@ -219,15 +240,11 @@ void multi_query_kernel(const Params p) {
   for (int t = 0; t < S::DT; ++t) acc[t] = f32x16{};
   float m = neg_inf(), l = 0.f;
 
-  auto compute = [&](int kb, int buf) {
-    const char* kl = s_k[buf];
-    const char* vl = s_v[buf];
-    f32x16 sc = f32x16{};
-#pragma unroll
-    for (int s = 0; s < S::KS; ++s) {
-      const bf16x8 a = *(const bf16x8*)(kl + i * S::KRS + 16 * (2 * s + hh));
-      sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qop[s], sc, 0, 0, 0);
-    }
+  // P^T operands of the current block (key steps 0 and 1).
+  bf16x8 pb[2];
+  // Online softmax of block kb: updates (m, l), rescales acc when m moves and leaves
+  // the block's P^T operands in pb.
+  auto softmax = [&](int kb, int buf, const f32x16& sc) {
     // Lane 32h + i holds S^T[key 8(j/4) + 4h + j%4][row i], j < 16: page 0 for j < 8.
     float km0 = p.scale_log2, km1 = p.scale_log2, vm0 = 1.f, vm1 = 1.f;
     if constexpr (FP8) {
@@ -237,9 +254,11 @@ void multi_query_kernel(const Params p) {
       vm1 = s_scale[buf][3];
     }
     const int bad0 = s_bad[buf][0], bad1 = s_bad[buf][1];
+    // bf16: one positive factor for the whole block, so the maximum is taken on the
+    // raw scores and the factor enters the exponent's fma; fp8: per-page factors.
     float sv[16];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) sv[j] = sc[j] * (j < 8 ? km0 : km1);
+    for (int j = 0; j < 16; ++j) sv[j] = FP8 ? sc[j] * (j < 8 ? km0 : km1) : sc[j];
     if ((kb + 1) * kTile > Ew_full || bad0 || bad1) {
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
@@ -247,10 +266,12 @@ void multi_query_kernel(const Params p) {
         if (key >= lim || (j < 8 ? bad0 : bad1)) sv[j] = neg_inf();
       }
     }
-    float mx = sv[0];
+    float mx = fmaxf(fmaxf(sv[0], sv[1]), sv[2]);
 #pragma unroll
-    for (int j = 1; j < 16; ++j) mx = fmaxf(mx, sv[j]);
+    for (int j = 3; j < 15; j += 2) mx = fmaxf(fmaxf(mx, sv[j]), sv[j + 1]);
+    mx = fmaxf(mx, sv[15]);
     mx = fmaxf(mx, swap32(mx));
+    if constexpr (!FP8) mx *= km0;
     // Lazy rescale: the reference maximum moves only when a score exceeds it by
     // more than 2^kRescaleLog2 (always when it is still -inf and a score is not).
     // A row whose keys are all masked so far keeps m = -inf and alpha = 1.
@@ -263,14 +284,14 @@ void multi_query_kernel(const Params p) {
       for (int t = 0; t < S::DT; ++t) acc[t] *= alpha;
     }
     const float mu = (m == neg_inf()) ? 0.f : m;
+    const float fk = FP8 ? 1.f : km0;
     float pr[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
-      pr[j] = __builtin_amdgcn_exp2f(sv[j] - mu);
+      pr[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[j], fk, -mu));
       l += pr[j];
     }
     // P^T operand of key step kk: K position 8h + e is key 16kk + 8(e/4) + 4h + e%4.
-    bf16x8 pb[2];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
       const float vm = kk ? vm1 : vm0;
@@ -278,35 +299,66 @@ void multi_query_kernel(const Params p) {
                        pack_bf16(pr[8 * kk + 4] * vm, pr[8 * kk + 5] * vm), pack_bf16(pr[8 * kk + 6] * vm, pr[8 * kk + 7] * vm)};
       pb[kk] = __builtin_bit_cast(bf16x8, w);
     }
-    // V^T operand: the transpose read gives lane (16-lane group q, index c) the 4
-    // keys k0 .. k0+3 of column d = 16 (q & 1) + c of the tile, when lane c' of
-    // the group addresses key k0 + c'/4, columns 4 (c' % 4) .. +3.
-    const int lr = (lane & 15) >> 2, lc = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  };
+  // Operand reads.  K rows of block buffer `buf` for S^T = K Q^T: lane 32h + i
+  // reads key i, elements [16s + 8h, 16s + 8h + 8).  V^T operands: the transpose read gives lane (16-lane group q, index c) the 4 keys
+  // k0 .. k0+3 of column d = 16 (q & 1) + c of a 32-column tile, when lane c' of the
+  // group addresses key k0 + c'/4, columns 4 (c' % 4) .. +3; operand kk*DT + t is
+  // key step kk, column tile t.
+  auto read_k = [&](bf16x8* ka, int buf) {
+    const char* kl = s_k[buf] + i * S::KRS + 16 * hh;
+#pragma unroll
+    for (int s = 0; s < S::KS; ++s) ka[s] = *(const bf16x8*)(kl + 32 * s);
+  };
+  const int lr = (lane & 15) >> 2, lc = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  auto read_v = [&](bf16x8* va, int buf) {
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      const char* vr = vl + (16 * kk + 4 * hh + lr) * S::VRS;
+      const char* vr = s_v[buf] + (16 * kk + 4 * hh + lr) * S::VRS + 2 * lc;
 #pragma unroll
       for (int t = 0; t < S::DT; ++t) {
-        const bf16x4 x0 = lds_tr_read(vr + 2 * (32 * t + lc));
-        const bf16x4 x1 = lds_tr_read(vr + 8 * S::VRS + 2 * (32 * t + lc));
-        const bf16x8 a = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-        acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kk], acc[t], 0, 0, 0);
+        const bf16x4 x0 = lds_tr_read(vr + 64 * t);
+        const bf16x4 x1 = lds_tr_read(vr + 8 * S::VRS + 64 * t);
+        va[kk * S::DT + t] = bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
       }
     }
   };
+  static_assert(S::KS == 2 * S::DT, "as many V^T operands as score k-steps");
 
-  // 3. Key blocks: stage block kb + 1 while block kb is computed.
-  if (nkb > 0) {
-    stage_load(0);
-    stage_write(0);
-  }
+  // 3. Key blocks.  Blocks 0 .. PD-1 are loaded before the loop, block 0 is
+  //    written to LDS, and iteration kb loads block kb + PD (past the wave's keys
+  //    nothing is read, but the loads are issued so that every iteration has the
+  //    same loads in flight), computes block kb and writes block kb + 1 to the other
+  //    buffer.  The loop is unrolled PD times so that each register set is fixed.
+#pragma unroll
+  for (int u = 0; u < PD; ++u) stage_load(u, u, page_id(u));
+  int pid_next = page_id(PD);
+  stage_write(0, 0);
   __syncthreads();
-  for (int kb = 0; kb < nkb; ++kb) {
-    const int buf = kb & 1;
-    if (kb + 1 < nkb) stage_load(kb + 1);
-    if (kb * kTile < Ew) compute(kb, buf);
-    if (kb + 1 < nkb) stage_write(buf ^ 1);
-    __syncthreads();
+  for (int kb0 = 0; kb0 < nkb; kb0 += PD) {
+#pragma unroll
+    for (int u = 0; u < PD; ++u) {
+      const int kb = kb0 + u;
+      if (kb < nkb) {
+        const int buf = kb & 1;
+        stage_load(kb + PD, u, pid_next);
+        pid_next = page_id(kb + PD + 1);
+        if (kb * kTile < Ew) {
+          bf16x8 ka[S::KS], va[S::KS];
+          read_k(ka, buf);
+          f32x16 sc = f32x16{};
+#pragma unroll
+          for (int s = 0; s < S::KS; ++s) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[s], qop[s], sc, 0, 0, 0);
+          softmax(kb, buf, sc);
+          read_v(va, buf);
+#pragma unroll
+          for (int s = 0; s < S::KS; ++s)
+            acc[s % S::DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[s], pb[s / S::DT], acc[s % S::DT], 0, 0, 0);
+        }
+        if (kb + 1 < nkb) stage_write((u + 1) % PD, buf ^ 1);
+        __syncthreads();
+      }
+    }
   }
 
   // 4. Normalise and write: lane 32h + i holds O^T[d = 32t + 8jj + 4h + 0..3][row i].
