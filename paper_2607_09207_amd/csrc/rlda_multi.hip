@@ -45,12 +45,17 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 #ifndef RLDA_MQ_VPAD
 #define RLDA_MQ_VPAD 32                       // ... of the V block
 #endif
-constexpr int kTile = 32;                     // query rows per wave = keys per block
+constexpr int kTile = 32;                     // rows of one MFMA tile = keys per block
+constexpr int kNT = kMultiTiles;              // 32-row tiles per wave
 constexpr int kBufs = 2;                      // LDS block buffers
+#ifndef RLDA_MQ_WAVES
+#define RLDA_MQ_WAVES (3 - kNT)               // waves per SIMD (register budget 512 / waves)
+#endif
+constexpr int kMqWaves = RLDA_MQ_WAVES;
 #ifndef RLDA_MQ_PREFETCH
 #define RLDA_MQ_PREFETCH 2                    // blocks loaded ahead into registers
 #endif
-static_assert(kTile * kWaves == kMultiRows, "a workgroup's rows are its waves' tiles");
+static_assert(kTile * kNT * kWaves == kMultiRows, "a workgroup's rows are its waves' tiles");
 
 template <int D, bool FP8>
 struct MqShape {
@@ -71,7 +76,7 @@ __device__ __forceinline__ bf16x4 lds_tr_read(const char* p) {
 }
 
 template <int D, bool FP8>
-__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(2, 2)))
+__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(kMqWaves, kMqWaves)))
 void multi_query_kernel(const Params p) {
   using S = MqShape<D, FP8>;
   // Two block buffers: block kb is computed from one while block kb + 1 is written
@@ -149,26 +154,34 @@ void multi_query_kernel(const Params p) {
   const int base_pos = L - n;                                   // position of query token 0
   const int E = max(0, base_pos + (r1 - 1) / G + 1);            // keys the workgroup reads
   const int nkb = (E + kTile - 1) / kTile;
-  const int wr0 = r0 + kTile * wave, wr1 = min(wr0 + kTile, r1);
+  const int wr0 = r0 + kTile * kNT * wave, wr1 = min(wr0 + kTile * kNT, r1);
   const int Ew = wr0 < wr1 ? max(0, base_pos + (wr1 - 1) / G + 1) : 0;       // keys this wave needs
   const int Ew_full = wr0 < wr1 ? max(0, base_pos + wr0 / G + 1) : 0;       // ... visible to all its rows
 
-  // This lane's query row: lanes i and i + 32 share row wr0 + i.
+  // This lane's query rows, one per tile: lanes i and i + 32 share row wr0 + 32 t + i.
   const int i = lane & 31, hh = lane >> 5;
-  const int row = wr0 + i;
-  const bool live = row < wr1;
-  const int qi = live ? row / G : 0;
-  const int head = live ? s_qh[g * G + (row - qi * G)] : 0;
-  const int lim = live ? base_pos + qi + 1 : 0;                 // keys [0, lim) are visible
+  bool live[kNT];
+  int qi[kNT], head[kNT], lim[kNT];
+#pragma unroll
+  for (int t = 0; t < kNT; ++t) {
+    const int row = wr0 + kTile * t + i;
+    live[t] = row < wr1;
+    qi[t] = live[t] ? row / G : 0;
+    head[t] = live[t] ? s_qh[g * G + (row - qi[t] * G)] : 0;
+    lim[t] = live[t] ? base_pos + qi[t] + 1 : 0;               // keys [0, lim) are visible
+  }
 
-  // Q operand (B of K Q^T): lane 32h + i holds row i's elements [16s + 8h, 16s + 8h + 8).
-  bf16x8 qop[S::KS];
+  // Q operands (B of K Q^T): lane 32h + i holds its row's elements [16s + 8h, 16s + 8h + 8).
+  bf16x8 qop[kNT][S::KS];
   {
     const __amdgpu_buffer_rsrc_t rq = make_rsrc_uni(p.q, (uint32_t)p.total_q * (uint32_t)Hq * D * 2u);
-    const int off = live ? ((q0 + qi) * Hq + head) * D * 2 : kPastRange;
 #pragma unroll
-    for (int s = 0; s < S::KS; ++s)
-      qop[s] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rq, off + 16 * (2 * s + hh), 0, 0));
+    for (int t = 0; t < kNT; ++t) {
+      const int off = live[t] ? ((q0 + qi[t]) * Hq + head[t]) * D * 2 : kPastRange;
+#pragma unroll
+      for (int s = 0; s < S::KS; ++s)
+        qop[t][s] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rq, off + 16 * (2 * s + hh), 0, 0));
+    }
   }
 
   // Staging: wave w brings page (w & 1) of each block's K (w < 2) or V (w >= 2).
@@ -235,16 +248,21 @@ void multi_query_kernel(const Params p) {
     }
   };
 
-  f32x16 acc[S::DT];
+  f32x16 acc[kNT][S::DT];
+  float m[kNT], l[kNT];
 #pragma unroll
-  for (int t = 0; t < S::DT; ++t) acc[t] = f32x16{};
-  float m = neg_inf(), l = 0.f;
+  for (int t = 0; t < kNT; ++t) {
+#pragma unroll
+    for (int c = 0; c < S::DT; ++c) acc[t][c] = f32x16{};
+    m[t] = neg_inf();
+    l[t] = 0.f;
+  }
 
-  // P^T operands of the current block (key steps 0 and 1).
-  bf16x8 pb[2];
-  // Online softmax of block kb: updates (m, l), rescales acc when m moves and leaves
-  // the block's P^T operands in pb.
-  auto softmax = [&](int kb, int buf, const f32x16& sc) {
+  // P^T operands of the current block per tile (key steps 0 and 1).
+  bf16x8 pb[kNT][2];
+  // Online softmax of tile t on block kb: updates (m, l), rescales the tile's
+  // accumulators when m moves and leaves the block's P^T operands in pb[t].
+  auto softmax = [&](int t, int kb, int buf, const f32x16& sc) {
     // Lane 32h + i holds S^T[key 8(j/4) + 4h + j%4][row i], j < 16: page 0 for j < 8.
     float km0 = p.scale_log2, km1 = p.scale_log2, vm0 = 1.f, vm1 = 1.f;
     if constexpr (FP8) {
@@ -263,7 +281,7 @@ void multi_query_kernel(const Params p) {
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const int key = kb * kTile + 8 * (j >> 2) + 4 * hh + (j & 3);
-        if (key >= lim || (j < 8 ? bad0 : bad1)) sv[j] = neg_inf();
+        if (key >= lim[t] || (j < 8 ? bad0 : bad1)) sv[j] = neg_inf();
       }
     }
     float mx = fmaxf(fmaxf(sv[0], sv[1]), sv[2]);
@@ -275,21 +293,21 @@ void multi_query_kernel(const Params p) {
     // Lazy rescale: the reference maximum moves only when a score exceeds it by
     // more than 2^kRescaleLog2 (always when it is still -inf and a score is not).
     // A row whose keys are all masked so far keeps m = -inf and alpha = 1.
-    const bool up = mx > m + kRescaleLog2;
+    const bool up = mx > m[t] + kRescaleLog2;
     if (__builtin_amdgcn_ballot_w64(up) != 0) {
-      const float alpha = up ? __builtin_amdgcn_exp2f(m - mx) : 1.f;
-      l *= alpha;
-      m = up ? mx : m;
+      const float alpha = up ? __builtin_amdgcn_exp2f(m[t] - mx) : 1.f;
+      l[t] *= alpha;
+      m[t] = up ? mx : m[t];
 #pragma unroll
-      for (int t = 0; t < S::DT; ++t) acc[t] *= alpha;
+      for (int c = 0; c < S::DT; ++c) acc[t][c] *= alpha;
     }
-    const float mu = (m == neg_inf()) ? 0.f : m;
+    const float mu = (m[t] == neg_inf()) ? 0.f : m[t];
     const float fk = FP8 ? 1.f : km0;
     float pr[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
       pr[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[j], fk, -mu));
-      l += pr[j];
+      l[t] += pr[j];
     }
     // P^T operand of key step kk: K position 8h + e is key 16kk + 8(e/4) + 4h + e%4.
 #pragma unroll
@@ -297,7 +315,7 @@ void multi_query_kernel(const Params p) {
       const float vm = kk ? vm1 : vm0;
       const u32x4 w = {pack_bf16(pr[8 * kk] * vm, pr[8 * kk + 1] * vm), pack_bf16(pr[8 * kk + 2] * vm, pr[8 * kk + 3] * vm),
                        pack_bf16(pr[8 * kk + 4] * vm, pr[8 * kk + 5] * vm), pack_bf16(pr[8 * kk + 6] * vm, pr[8 * kk + 7] * vm)};
-      pb[kk] = __builtin_bit_cast(bf16x8, w);
+      pb[t][kk] = __builtin_bit_cast(bf16x8, w);
     }
   };
   // Operand reads.  K rows of block buffer `buf` for S^T = K Q^T: lane 32h + i
@@ -344,16 +362,25 @@ void multi_query_kernel(const Params p) {
         stage_load(kb + PD, u, pid_next);
         pid_next = page_id(kb + PD + 1);
         if (kb * kTile < Ew) {
+          // Each K and V operand read serves every tile of the wave.
           bf16x8 ka[S::KS], va[S::KS];
           read_k(ka, buf);
-          f32x16 sc = f32x16{};
+          f32x16 sc[kNT];
 #pragma unroll
-          for (int s = 0; s < S::KS; ++s) sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[s], qop[s], sc, 0, 0, 0);
-          softmax(kb, buf, sc);
+          for (int t = 0; t < kNT; ++t) sc[t] = f32x16{};
+#pragma unroll
+          for (int s = 0; s < S::KS; ++s)
+#pragma unroll
+            for (int t = 0; t < kNT; ++t) sc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[s], qop[t][s], sc[t], 0, 0, 0);
+#pragma unroll
+          for (int t = 0; t < kNT; ++t) softmax(t, kb, buf, sc[t]);
           read_v(va, buf);
 #pragma unroll
           for (int s = 0; s < S::KS; ++s)
-            acc[s % S::DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[s], pb[s / S::DT], acc[s % S::DT], 0, 0, 0);
+#pragma unroll
+            for (int t = 0; t < kNT; ++t)
+              acc[t][s % S::DT] =
+                  __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[s], pb[t][s / S::DT], acc[t][s % S::DT], 0, 0, 0);
         }
         if (kb + 1 < nkb) stage_write((u + 1) % PD, buf ^ 1);
         __syncthreads();
@@ -361,23 +388,26 @@ void multi_query_kernel(const Params p) {
     }
   }
 
-  // 4. Normalise and write: lane 32h + i holds O^T[d = 32t + 8jj + 4h + 0..3][row i].
-  const float lt = l + swap32(l);
-  if (!live) return;
-  const float inv = lt > 0.f ? 1.f / lt : 0.f;
-  const int64_t ob = ((int64_t)(q0 + qi) * Hq + head) * D;
+  // 4. Normalise and write: lane 32h + i holds O^T[d = 32c + 8jj + 4h + 0..3][its row].
 #pragma unroll
-  for (int t = 0; t < S::DT; ++t)
+  for (int t = 0; t < kNT; ++t) {
+    const float lt = l[t] + swap32(l[t]);
+    if (!live[t]) continue;
+    const float inv = lt > 0.f ? 1.f / lt : 0.f;
+    const int64_t ob = ((int64_t)(q0 + qi[t]) * Hq + head[t]) * D;
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      const int d = 32 * t + 8 * jj + 4 * hh;
-      const float o0 = acc[t][4 * jj] * inv, o1 = acc[t][4 * jj + 1] * inv;
-      const float o2 = acc[t][4 * jj + 2] * inv, o3 = acc[t][4 * jj + 3] * inv;
-      if (p.out_bf16)
-        *(u32x2*)((uint16_t*)p.out + ob + d) = u32x2{pack_bf16(o0, o1), pack_bf16(o2, o3)};
-      else
-        *(f32x4*)((float*)p.out + ob + d) = f32x4{o0, o1, o2, o3};
-    }
+    for (int c = 0; c < S::DT; ++c)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int d = 32 * c + 8 * jj + 4 * hh;
+        const float o0 = acc[t][c][4 * jj] * inv, o1 = acc[t][c][4 * jj + 1] * inv;
+        const float o2 = acc[t][c][4 * jj + 2] * inv, o3 = acc[t][c][4 * jj + 3] * inv;
+        if (p.out_bf16)
+          *(u32x2*)((uint16_t*)p.out + ob + d) = u32x2{pack_bf16(o0, o1), pack_bf16(o2, o3)};
+        else
+          *(f32x4*)((float*)p.out + ob + d) = f32x4{o0, o1, o2, o3};
+      }
+  }
 }
 
 template <int D, bool FP8>

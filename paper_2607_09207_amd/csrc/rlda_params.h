@@ -75,7 +75,11 @@ int launch_grouped(KvKind kind, int head_dim, int group, const Params& p, int ng
 int launch_append(KvKind kind, int head_dim, const Params& p, void* stream);
 // Multi-token queries (rlda_multi.hip): one workgroup per (128-row query block, KV head).
 int launch_multi(KvKind kind, int head_dim, const Params& p, int grid, void* stream, void* ev_begin, void* ev_end);
-constexpr int kMultiRows = 128;    // query rows (token, head pairs) per workgroup of the multi-token kernel
+#ifndef RLDA_MQ_TILES
+#define RLDA_MQ_TILES 1            // 32-row MFMA tiles per wave in the multi-token kernel
+#endif
+constexpr int kMultiTiles = RLDA_MQ_TILES;
+constexpr int kMultiRows = 128 * kMultiTiles;   // query rows (token, head pairs) per workgroup of the multi-token kernel
 constexpr int kMultiMaxBatch = 4096;   // its per-sequence LDS table stays within 64 KiB of LDS per workgroup
 
 }  // namespace rlda
