@@ -52,6 +52,7 @@ constexpr int kBufs = 2;                      // LDS block buffers
 #define RLDA_MQ_WAVES (3 - kNT)               // waves per SIMD (register budget 512 / waves)
 #endif
 constexpr int kMqWaves = RLDA_MQ_WAVES;
+
 #ifndef RLDA_MQ_PREFETCH
 #define RLDA_MQ_PREFETCH 2                    // blocks loaded ahead into registers
 #endif
@@ -68,8 +69,17 @@ struct MqShape {
   static constexpr int LPL = kPage * CPR / 64; // 16-byte loads per lane to stage one page
 };
 
-// Exchange with the lane 32 away (the other half of a score row).
-__device__ __forceinline__ float swap32(float x) { return __shfl_xor(x, 32); }
+// Max / sum of a value with the one 32 lanes away (the other half of a score
+// row), both halves getting the result: v_permlane32_swap of x with itself leaves
+// the lower halves of x in one result and the upper halves in the other.
+__device__ __forceinline__ float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 __device__ __forceinline__ bf16x4 lds_tr_read(const char* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(__attribute__((address_space(3))) char*)p);
@@ -288,7 +298,7 @@ void multi_query_kernel(const Params p) {
 #pragma unroll
     for (int j = 3; j < 15; j += 2) mx = fmaxf(fmaxf(mx, sv[j]), sv[j + 1]);
     mx = fmaxf(mx, sv[15]);
-    mx = fmaxf(mx, swap32(mx));
+    mx = pair_max(mx);
     if constexpr (!FP8) mx *= km0;
     // Lazy rescale: the reference maximum moves only when a score exceeds it by
     // more than 2^kRescaleLog2 (always when it is still -inf and a score is not).
@@ -372,9 +382,9 @@ void multi_query_kernel(const Params p) {
           for (int s = 0; s < S::KS; ++s)
 #pragma unroll
             for (int t = 0; t < kNT; ++t) sc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[s], qop[t][s], sc[t], 0, 0, 0);
+          read_v(va, buf);   // independent of the softmax: its latency overlaps it
 #pragma unroll
           for (int t = 0; t < kNT; ++t) softmax(t, kb, buf, sc[t]);
-          read_v(va, buf);
 #pragma unroll
           for (int s = 0; s < S::KS; ++s)
 #pragma unroll
@@ -391,7 +401,7 @@ void multi_query_kernel(const Params p) {
   // 4. Normalise and write: lane 32h + i holds O^T[d = 32c + 8jj + 4h + 0..3][its row].
 #pragma unroll
   for (int t = 0; t < kNT; ++t) {
-    const float lt = l[t] + swap32(l[t]);
+    const float lt = pair_sum(l[t]);
     if (!live[t]) continue;
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
     const int64_t ob = ((int64_t)(q0 + qi[t]) * Hq + head[t]) * D;
