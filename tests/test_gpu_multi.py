@@ -137,3 +137,15 @@ def test_multi_is_bitwise_deterministic(torch_cuda):
     a, _ = run_multi(torch_cuda, w, handle=h, tag="det 1")
     b, _ = run_multi(torch_cuda, w, handle=h, tag="det 2")
     assert np.array_equal(a, b)
+
+
+def test_maximum_batch_multi(torch_cuda):
+    """The multi-token entry point's largest batch (4096) with 0-3 rows per sequence."""
+    rng = np.random.default_rng(79)
+    lens = rng.integers(1, 41, size=4096)
+    ql = np.minimum(rng.integers(0, 4, size=4096), lens)
+    w = I.make_multi(lens.tolist(), ql.tolist(), 8, 2, 128, q_dtype="bf16", kv_dtype="bf16", seed=80,
+                     max_pages_per_seq=3)
+    got, flags = run_multi(torch_cuda, w, tag="max batch multi")
+    assert flags == 0
+    assert_close(got, oracle.run_multi(w), "bf16", "multi max batch 4096")

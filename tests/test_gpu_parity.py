@@ -311,3 +311,14 @@ def test_split_merge_handoff_under_repetition(torch_cuda):
         bad += int(not torch.equal(out, ref_b))
     torch.cuda.synchronize()
     assert bad == 0
+
+
+def test_maximum_batch(torch_cuda):
+    """kMaxBatch = 8192 sequences (short and empty ones mixed): the LDS prefix sums
+    and the stream decode cover the largest batch the library accepts."""
+    rng = np.random.default_rng(77)
+    lens = rng.integers(0, 41, size=8192)
+    w = I.make_custom(lens.tolist(), 8, 2, 128, q_dtype="bf16", kv_dtype="bf16", seed=78, max_pages_per_seq=3)
+    got, flags = gpu_run(torch_cuda, w, tag="max batch")
+    assert flags == 0
+    assert_close(got, oracle.run(w), "bf16", "max batch 8192")
