@@ -45,17 +45,31 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 #ifndef RLDA_MQ_VPAD
 #define RLDA_MQ_VPAD 32                       // ... of the V block
 #endif
-constexpr int kTile = 32;                     // rows of one MFMA tile = keys per block
+constexpr int kTile = 32;                     // rows (and keys) of one MFMA tile
 constexpr int kNT = kMultiTiles;              // 32-row tiles per wave
-constexpr int kBufs = 2;                      // LDS block buffers
-#ifndef RLDA_MQ_WAVES
-#define RLDA_MQ_WAVES (3 - kNT)               // waves per SIMD (register budget 512 / waves)
+#ifndef RLDA_MQ_KEY_TILES
+#define RLDA_MQ_KEY_TILES 1                   // 32-key score tiles per key block
 #endif
-constexpr int kMqWaves = RLDA_MQ_WAVES;
+constexpr int kKH = RLDA_MQ_KEY_TILES;
+constexpr int kKeys = kTile * kKH;            // keys per block (2 kKH pages)
 
 #ifndef RLDA_MQ_PREFETCH
-#define RLDA_MQ_PREFETCH 2                    // blocks loaded ahead into registers
+#define RLDA_MQ_PREFETCH 2                    // blocks loaded ahead into registers (register staging)
 #endif
+#ifndef RLDA_MQ_DMA
+#define RLDA_MQ_DMA 1                         // bf16, d = 128: pages go to LDS by buffer-load DMA
+#endif
+
+// Workgroup barrier for the DMA path: wait until at most N vector-memory
+// operations of this wave are outstanding (the DMAs of the newest block) and its
+// LDS operations are done, then s_barrier.  __syncthreads would wait for every
+// outstanding DMA (its release fence counts them as stores).  The asm's memory
+// clobber keeps the compiler from moving memory accesses across it.
+template <int N>
+__device__ __forceinline__ void dma_barrier() {
+  static_assert(N >= 0 && N < 16, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
 static_assert(kTile * kNT * kWaves == kMultiRows, "a workgroup's rows are its waves' tiles");
 
 template <int D, bool FP8>
@@ -63,8 +77,24 @@ struct MqShape {
   static constexpr int KS = D / 16;           // 32x32x16 k-steps of K Q^T
   static constexpr int DT = D / 32;           // 32-wide output tiles of O^T
   static constexpr int EB = FP8 ? 1 : 2;      // bytes per cached element
-  static constexpr int KRS = 2 * D + RLDA_MQ_KPAD;   // LDS row stride of the K block (bytes, bf16 rows)
-  static constexpr int VRS = 2 * D + RLDA_MQ_VPAD;   // ... of the V block
+  // bf16 pages at d = 128 are copied to LDS by the buffer-load DMA (no registers,
+  // no LDS writes by the waves) into unpadded rows whose 16-byte chunks are
+  // permuted per row (see chunk_pos); other caches are staged through registers
+  // (fp8 is converted on the way) into padded rows.
+  static constexpr bool DMA = !FP8 && D == 128 && RLDA_MQ_DMA;
+  static constexpr int NBUF = DMA ? 3 : 2;    // LDS block buffers
+  // Waves per SIMD (register budget 512 / waves).  Without staging registers the
+  // DMA path fits three (167 registers) when the V operands are read after the
+  // softmax; the register path keeps two and reads V before the softmax, where
+  // the read latency overlaps it.
+#ifdef RLDA_MQ_WAVES
+  static constexpr int WAVES = RLDA_MQ_WAVES;
+#else
+  static constexpr int WAVES = kNT == 1 ? (DMA ? 3 : 2) : 1;
+#endif
+  static constexpr bool V_EARLY = !DMA;
+  static constexpr int KRS = DMA ? 2 * D : 2 * D + RLDA_MQ_KPAD;   // LDS row stride of the K block (bytes)
+  static constexpr int VRS = DMA ? 2 * D : 2 * D + RLDA_MQ_VPAD;   // ... of the V block
   static constexpr int CPR = D * EB / 16;     // 16-byte chunks per cached row
   static constexpr int LPL = kPage * CPR / 64; // 16-byte loads per lane to stage one page
 };
@@ -86,15 +116,16 @@ __device__ __forceinline__ bf16x4 lds_tr_read(const char* p) {
 }
 
 template <int D, bool FP8>
-__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(kMqWaves, kMqWaves)))
+__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads),
+                          amdgpu_waves_per_eu(MqShape<D, FP8>::WAVES, MqShape<D, FP8>::WAVES)))
 void multi_query_kernel(const Params p) {
   using S = MqShape<D, FP8>;
   // Two block buffers: block kb is computed from one while block kb + 1 is written
   // to the other.
-  __shared__ __align__(16) char s_k[kBufs][kTile * S::KRS];
-  __shared__ __align__(16) char s_v[kBufs][kTile * S::VRS];
-  __shared__ float s_scale[kBufs][4];   // fp8: K scales of the block's pages 0, 1; then V's
-  __shared__ int32_t s_bad[kBufs][2];   // page of the block not in the pool (contributes nothing)
+  __shared__ __align__(16) char s_k[S::NBUF][kKeys * S::KRS];
+  __shared__ __align__(16) char s_v[S::NBUF][kKeys * S::VRS];
+  __shared__ float s_scale[S::NBUF][4 * kKH];   // fp8: K scales of the block's pages, then V's
+  __shared__ int32_t s_bad[S::NBUF][2 * kKH];   // page of the block not in the pool (contributes nothing)
   __shared__ int32_t s_scan[kWaves];
   __shared__ int16_t s_qh[kMaxQHeads];
   extern __shared__ int32_t s_rb[];     // [batch + 1]: row blocks of the sequences before b
@@ -163,7 +194,7 @@ void multi_query_kernel(const Params p) {
   const int r0 = rb * kMultiRows, r1 = min(r0 + kMultiRows, rows);
   const int base_pos = L - n;                                   // position of query token 0
   const int E = max(0, base_pos + (r1 - 1) / G + 1);            // keys the workgroup reads
-  const int nkb = (E + kTile - 1) / kTile;
+  const int nkb = (E + kKeys - 1) / kKeys;
   const int wr0 = r0 + kTile * kNT * wave, wr1 = min(wr0 + kTile * kNT, r1);
   const int Ew = wr0 < wr1 ? max(0, base_pos + (wr1 - 1) / G + 1) : 0;       // keys this wave needs
   const int Ew_full = wr0 < wr1 ? max(0, base_pos + wr0 / G + 1) : 0;       // ... visible to all its rows
@@ -194,67 +225,112 @@ void multi_query_kernel(const Params p) {
     }
   }
 
-  // Staging: wave w brings page (w & 1) of each block's K (w < 2) or V (w >= 2).
+  // Staging: wave w brings pages (w & 1) + 2h, h < kKH, of each block's K (w < 2)
+  // or V (w >= 2).
   const int which = wave >> 1, pgw = wave & 1;
   const char* pool = (const char*)(which ? p.v : p.k);
   const float* scl = which ? p.v_scale : p.k_scale;
   // Register sets of the blocks in flight: block kb is loaded into set kb % PD
   // PD blocks before it is computed (global latency is several blocks' work).
   constexpr int PD = RLDA_MQ_PREFETCH;
-  u32x4 stg[PD][S::LPL];
-  float stg_scale[PD];
-  int stg_bad[PD];
+  u32x4 stg[PD][kKH][S::LPL];
+  float stg_scale[PD][kKH];
+  int stg_bad[PD][kKH];
   // Page ids come through the scalar cache (the block table is read-only here),
   // one block ahead of the loads that use them; the index is clamped into the row
   // so the load is always in bounds (pages past the keys are not used).
   typedef const __attribute__((address_space(4))) int32_t bt_elem;
   bt_elem* bt_row = (bt_elem*)(const void*)(p.block_table + (int64_t)b * p.max_pages);
-  auto page_id = [&](int kb) { return bt_row[min(2 * kb + pgw, p.max_pages - 1)]; };
-  auto stage_load = [&](int kb, int set, int pid) {
-    const int j = 2 * kb + pgw;   // page index in the sequence
-    int tok = min(max(E - j * kPage, 0), kPage);
-    stg_bad[set] = 0;
-    if (tok > 0) {
-      if ((unsigned)pid >= (unsigned)p.num_pages) {
-        if (lane == 0) atomicOr(p.flags, kFlagBadPage);
-        tok = 0;
-        stg_bad[set] = 1;
-      }
-    }
-    const int64_t po = tok > 0 ? (int64_t)pid * p.stride_page + (int64_t)g * p.stride_head : 0;
-    const uint32_t nrec = tok > 0 ? (uint32_t)((tok - 1) * p.stride_slot + D * S::EB) : 0u;
-    const __amdgpu_buffer_rsrc_t r = make_rsrc_uni(pool + po, nrec);
+  auto page_index = [&](int kb, int h) { return 2 * kKH * kb + pgw + 2 * h; };
+  auto page_ids = [&](int kb, int* pid) {
 #pragma unroll
-    for (int k = 0; k < S::LPL; ++k) {
-      const int ci = lane + 64 * k, rr = ci / S::CPR, c = ci % S::CPR;
-      stg[set][k] = __builtin_amdgcn_raw_buffer_load_b128(r, rr * p.stride_slot + 16 * c, 0, 0);
+    for (int h = 0; h < kKH; ++h) pid[h] = bt_row[min(page_index(kb, h), p.max_pages - 1)];
+  };
+  auto stage_load = [&](int kb, int set, const int* pid) {
+#pragma unroll
+    for (int h = 0; h < kKH; ++h) {
+      const int j = page_index(kb, h);   // page index in the sequence
+      int tok = min(max(E - j * kPage, 0), kPage);
+      stg_bad[set][h] = 0;
+      if (tok > 0) {
+        if ((unsigned)pid[h] >= (unsigned)p.num_pages) {
+          if (lane == 0) atomicOr(p.flags, kFlagBadPage);
+          tok = 0;
+          stg_bad[set][h] = 1;
+        }
+      }
+      const int64_t po = tok > 0 ? (int64_t)pid[h] * p.stride_page + (int64_t)g * p.stride_head : 0;
+      const uint32_t nrec = tok > 0 ? (uint32_t)((tok - 1) * p.stride_slot + D * S::EB) : 0u;
+      const __amdgpu_buffer_rsrc_t r = make_rsrc_uni(pool + po, nrec);
+#pragma unroll
+      for (int k = 0; k < S::LPL; ++k) {
+        const int ci = lane + 64 * k, rr = ci / S::CPR, c = ci % S::CPR;
+        stg[set][h][k] = __builtin_amdgcn_raw_buffer_load_b128(r, rr * p.stride_slot + 16 * c, 0, 0);
+      }
+      if constexpr (FP8) stg_scale[set][h] = tok > 0 ? scl[(int64_t)pid[h] * Hkv + g] : 0.f;
     }
-    if constexpr (FP8) stg_scale[set] = tok > 0 ? scl[(int64_t)pid * Hkv + g] : 0.f;
   };
   auto stage_write = [&](int set, int buf) {
     char* dst = which ? s_v[buf] : s_k[buf];
     const int RS = which ? S::VRS : S::KRS;
 #pragma unroll
-    for (int k = 0; k < S::LPL; ++k) {
-      const int ci = lane + 64 * k, rr = ci / S::CPR, c = ci % S::CPR;
-      char* rowp = dst + (kPage * pgw + rr) * RS;
-      if constexpr (!FP8) {
-        *(u32x4*)(rowp + 16 * c) = stg[set][k];
-      } else {   // 16 E4M3 values -> 16 bf16 (exact)
-        uint32_t w[8];
+    for (int h = 0; h < kKH; ++h) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const f32x2 a = fp8x2_to_f32(stg[set][k][e], false), bb = fp8x2_to_f32(stg[set][k][e], true);
-          w[2 * e] = pack_bf16(a[0], a[1]);
-          w[2 * e + 1] = pack_bf16(bb[0], bb[1]);
+      for (int k = 0; k < S::LPL; ++k) {
+        const int ci = lane + 64 * k, rr = ci / S::CPR, c = ci % S::CPR;
+        char* rowp = dst + (kPage * (pgw + 2 * h) + rr) * RS;
+        if constexpr (!FP8) {
+          *(u32x4*)(rowp + 16 * c) = stg[set][h][k];
+        } else {   // 16 E4M3 values -> 16 bf16 (exact)
+          uint32_t w[8];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const f32x2 a = fp8x2_to_f32(stg[set][h][k][e], false), bb = fp8x2_to_f32(stg[set][h][k][e], true);
+            w[2 * e] = pack_bf16(a[0], a[1]);
+            w[2 * e + 1] = pack_bf16(bb[0], bb[1]);
+          }
+          *(u32x4*)(rowp + 32 * c) = u32x4{w[0], w[1], w[2], w[3]};
+          *(u32x4*)(rowp + 32 * c + 16) = u32x4{w[4], w[5], w[6], w[7]};
         }
-        *(u32x4*)(rowp + 32 * c) = u32x4{w[0], w[1], w[2], w[3]};
-        *(u32x4*)(rowp + 32 * c + 16) = u32x4{w[4], w[5], w[6], w[7]};
+      }
+      if (lane == 0) {
+        if constexpr (FP8) s_scale[buf][2 * kKH * which + pgw + 2 * h] = stg_scale[set][h];
+        if (which == 0) s_bad[buf][pgw + 2 * h] = stg_bad[set][h];
       }
     }
-    if (lane == 0) {
-      if constexpr (FP8) s_scale[buf][2 * which + pgw] = stg_scale[set];
-      if (which == 0) s_bad[buf][pgw] = stg_bad[set];
+  };
+
+  // DMA path: 16-byte chunk c of row r (the row's slot in its page) sits at chunk
+  // position c ^ (r & 15) in K rows and c ^ 4 (r & 3) in V rows, so that the
+  // score operand reads (16 rows, one chunk) and the transpose reads (4 rows, 4
+  // chunks, two 16-lane groups) each touch all 64 banks once.  Lane l of the k-th
+  // DMA of a page fills slot 64k + l of the page, row (64k + l) / 16, position
+  // (64k + l) % 16, so it fetches the chunk that belongs there.
+  auto chunk_pos = [](bool v_rows, int r, int c) { return c ^ (v_rows ? 4 * (r & 3) : (r & 15)); };
+  int bad_pages = 0;   // DMA path: the flag is raised after the loop (no atomics between the DMAs)
+  auto dma_issue = [&](int kb, int buf, const int* pid) {
+    char* dst = which ? s_v[buf] : s_k[buf];
+#pragma unroll
+    for (int h = 0; h < kKH; ++h) {
+      const int j = page_index(kb, h);
+      int tok = min(max(E - j * kPage, 0), kPage);
+      int badp = 0;
+      if (tok > 0 && (unsigned)pid[h] >= (unsigned)p.num_pages) {
+        tok = 0;
+        badp = 1;
+      }
+      bad_pages |= badp;
+      const int64_t po = tok > 0 ? (int64_t)pid[h] * p.stride_page + (int64_t)g * p.stride_head : 0;
+      const uint32_t nrec = tok > 0 ? (uint32_t)((tok - 1) * p.stride_slot + D * S::EB) : 0u;
+      const __amdgpu_buffer_rsrc_t r = make_rsrc_uni(pool + po, nrec);
+      char* page_base = dst + kPage * (pgw + 2 * h) * S::KRS;
+#pragma unroll
+      for (int k = 0; k < S::LPL; ++k) {
+        const int sl = 64 * k + lane, rr = sl / S::CPR, c = chunk_pos(which != 0, rr, sl % S::CPR);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            r, (__attribute__((address_space(3))) void*)(page_base + 1024 * k), 16, rr * p.stride_slot + 16 * c, 0, 0, 0);
+      }
+      if (which == 0 && lane == 0) s_bad[buf][pgw + 2 * h] = badp;
     }
   };
 
@@ -268,38 +344,45 @@ void multi_query_kernel(const Params p) {
     l[t] = 0.f;
   }
 
-  // P^T operands of the current block per tile (key steps 0 and 1).
-  bf16x8 pb[kNT][2];
+  // P^T operands of the current block per tile: key tile kh, key step kk.
+  bf16x8 pb[kNT][kKH][2];
   // Online softmax of tile t on block kb: updates (m, l), rescales the tile's
   // accumulators when m moves and leaves the block's P^T operands in pb[t].
-  auto softmax = [&](int t, int kb, int buf, const f32x16& sc) {
-    // Lane 32h + i holds S^T[key 8(j/4) + 4h + j%4][row i], j < 16: page 0 for j < 8.
-    float km0 = p.scale_log2, km1 = p.scale_log2, vm0 = 1.f, vm1 = 1.f;
-    if constexpr (FP8) {
-      km0 *= s_scale[buf][0];
-      km1 *= s_scale[buf][1];
-      vm0 = s_scale[buf][2];
-      vm1 = s_scale[buf][3];
+  auto softmax = [&](int t, int kb, int buf, const f32x16* sc) {
+    // Lane 32h + i holds S^T[key 32kh + 8(j/4) + 4h + j%4][row i] of key tile kh,
+    // j < 16: page 2kh for j < 8, 2kh + 1 above.
+    float km[2 * kKH], vm[2 * kKH];
+    int bad = 0;
+#pragma unroll
+    for (int q = 0; q < 2 * kKH; ++q) {
+      km[q] = FP8 ? p.scale_log2 * s_scale[buf][q] : p.scale_log2;
+      vm[q] = FP8 ? s_scale[buf][2 * kKH + q] : 1.f;
+      bad |= s_bad[buf][q];
     }
-    const int bad0 = s_bad[buf][0], bad1 = s_bad[buf][1];
     // bf16: one positive factor for the whole block, so the maximum is taken on the
     // raw scores and the factor enters the exponent's fma; fp8: per-page factors.
-    float sv[16];
+    float sv[kKH][16];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) sv[j] = FP8 ? sc[j] * (j < 8 ? km0 : km1) : sc[j];
-    if ((kb + 1) * kTile > Ew_full || bad0 || bad1) {
+    for (int kh = 0; kh < kKH; ++kh)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int key = kb * kTile + 8 * (j >> 2) + 4 * hh + (j & 3);
-        if (key >= lim[t] || (j < 8 ? bad0 : bad1)) sv[j] = neg_inf();
-      }
+      for (int j = 0; j < 16; ++j) sv[kh][j] = FP8 ? sc[kh][j] * km[2 * kh + (j >> 3)] : sc[kh][j];
+    if ((kb + 1) * kKeys > Ew_full || bad) {
+#pragma unroll
+      for (int kh = 0; kh < kKH; ++kh)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int key = kb * kKeys + kTile * kh + 8 * (j >> 2) + 4 * hh + (j & 3);
+          if (key >= lim[t] || s_bad[buf][2 * kh + (j >> 3)]) sv[kh][j] = neg_inf();
+        }
     }
-    float mx = fmaxf(fmaxf(sv[0], sv[1]), sv[2]);
+    float mx = neg_inf();
 #pragma unroll
-    for (int j = 3; j < 15; j += 2) mx = fmaxf(fmaxf(mx, sv[j]), sv[j + 1]);
-    mx = fmaxf(mx, sv[15]);
+    for (int kh = 0; kh < kKH; ++kh) {
+#pragma unroll
+      for (int j = 0; j < 16; j += 2) mx = fmaxf(fmaxf(mx, sv[kh][j]), sv[kh][j + 1]);
+    }
     mx = pair_max(mx);
-    if constexpr (!FP8) mx *= km0;
+    if constexpr (!FP8) mx *= km[0];
     // Lazy rescale: the reference maximum moves only when a score exceeds it by
     // more than 2^kRescaleLog2 (always when it is still -inf and a score is not).
     // A row whose keys are all masked so far keeps m = -inf and alpha = 1.
@@ -312,20 +395,24 @@ void multi_query_kernel(const Params p) {
       for (int c = 0; c < S::DT; ++c) acc[t][c] *= alpha;
     }
     const float mu = (m[t] == neg_inf()) ? 0.f : m[t];
-    const float fk = FP8 ? 1.f : km0;
-    float pr[16];
+    const float fk = FP8 ? 1.f : km[0];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      pr[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[j], fk, -mu));
-      l[t] += pr[j];
-    }
-    // P^T operand of key step kk: K position 8h + e is key 16kk + 8(e/4) + 4h + e%4.
+    for (int kh = 0; kh < kKH; ++kh) {
+      float pr[16];
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const float vm = kk ? vm1 : vm0;
-      const u32x4 w = {pack_bf16(pr[8 * kk] * vm, pr[8 * kk + 1] * vm), pack_bf16(pr[8 * kk + 2] * vm, pr[8 * kk + 3] * vm),
-                       pack_bf16(pr[8 * kk + 4] * vm, pr[8 * kk + 5] * vm), pack_bf16(pr[8 * kk + 6] * vm, pr[8 * kk + 7] * vm)};
-      pb[t][kk] = __builtin_bit_cast(bf16x8, w);
+      for (int j = 0; j < 16; ++j) {
+        pr[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[kh][j], fk, -mu));
+        l[t] += pr[j];
+      }
+      // P^T operand of key step kk: K position 8h + e is key 16kk + 8(e/4) + 4h + e%4
+      // of the key tile.
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const float v = vm[2 * kh + kk];
+        const u32x4 w = {pack_bf16(pr[8 * kk] * v, pr[8 * kk + 1] * v), pack_bf16(pr[8 * kk + 2] * v, pr[8 * kk + 3] * v),
+                         pack_bf16(pr[8 * kk + 4] * v, pr[8 * kk + 5] * v), pack_bf16(pr[8 * kk + 6] * v, pr[8 * kk + 7] * v)};
+        pb[t][kh][kk] = __builtin_bit_cast(bf16x8, w);
+      }
     }
   };
   // Operand reads.  K rows of block buffer `buf` for S^T = K Q^T: lane 32h + i
@@ -333,67 +420,131 @@ void multi_query_kernel(const Params p) {
   // k0 .. k0+3 of column d = 16 (q & 1) + c of a 32-column tile, when lane c' of the
   // group addresses key k0 + c'/4, columns 4 (c' % 4) .. +3; operand kk*DT + t is
   // key step kk, column tile t.
-  auto read_k = [&](bf16x8* ka, int buf) {
-    const char* kl = s_k[buf] + i * S::KRS + 16 * hh;
+  auto read_k = [&](bf16x8* ka, int buf, int kh) {
+    const int R = kTile * kh + i;
+    const char* kl = s_k[buf] + R * S::KRS;
 #pragma unroll
-    for (int s = 0; s < S::KS; ++s) ka[s] = *(const bf16x8*)(kl + 32 * s);
+    for (int s = 0; s < S::KS; ++s) {
+      const int c = 2 * s + hh;
+      ka[s] = *(const bf16x8*)(kl + 16 * (S::DMA ? chunk_pos(false, R, c) : c));
+    }
   };
   const int lr = (lane & 15) >> 2, lc = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  auto read_v = [&](bf16x8* va, int buf) {
+  auto read_v = [&](bf16x8* va, int buf, int kh) {
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      const char* vr = s_v[buf] + (16 * kk + 4 * hh + lr) * S::VRS + 2 * lc;
+      const int R = kTile * kh + 16 * kk + 4 * hh + lr;   // and R + 8: the same R & 3
+      const char* vr = s_v[buf] + R * S::VRS;
 #pragma unroll
       for (int t = 0; t < S::DT; ++t) {
-        const bf16x4 x0 = lds_tr_read(vr + 64 * t);
-        const bf16x4 x1 = lds_tr_read(vr + 8 * S::VRS + 64 * t);
+        // column 32t + lc: chunk (32t + lc) / 8, byte 2 ((32t + lc) % 8) = 8 (lane & 1) in it
+        const int c = 4 * t + (lc >> 3);
+        const int off = S::DMA ? 16 * chunk_pos(true, R, c) + 8 * (lane & 1) : 2 * (32 * t + lc);
+        const bf16x4 x0 = lds_tr_read(vr + off);
+        const bf16x4 x1 = lds_tr_read(vr + 8 * S::VRS + off);
         va[kk * S::DT + t] = bf16x8{x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
       }
     }
   };
   static_assert(S::KS == 2 * S::DT, "as many V^T operands as score k-steps");
 
-  // 3. Key blocks.  Blocks 0 .. PD-1 are loaded before the loop, block 0 is
-  //    written to LDS, and iteration kb loads block kb + PD (past the wave's keys
-  //    nothing is read, but the loads are issued so that every iteration has the
-  //    same loads in flight), computes block kb and writes block kb + 1 to the other
-  //    buffer.  The loop is unrolled PD times so that each register set is fixed.
+  // Block kb in LDS buffer buf: scores, softmax, P V, for the wave's row tiles.
+  auto compute_block = [&](int kb, int buf) {
+    if (kb * kKeys < Ew) {
+      // Each K and V operand read serves every row tile of the wave.
+      f32x16 sc[kNT][kKH];
+      bf16x8 va[kKH][S::KS];
 #pragma unroll
-  for (int u = 0; u < PD; ++u) stage_load(u, u, page_id(u));
-  int pid_next = page_id(PD);
-  stage_write(0, 0);
-  __syncthreads();
-  for (int kb0 = 0; kb0 < nkb; kb0 += PD) {
+      for (int kh = 0; kh < kKH; ++kh) {
+        bf16x8 ka[S::KS];
+        read_k(ka, buf, kh);
 #pragma unroll
-    for (int u = 0; u < PD; ++u) {
-      const int kb = kb0 + u;
-      if (kb < nkb) {
-        const int buf = kb & 1;
-        stage_load(kb + PD, u, pid_next);
-        pid_next = page_id(kb + PD + 1);
-        if (kb * kTile < Ew) {
-          // Each K and V operand read serves every tile of the wave.
-          bf16x8 ka[S::KS], va[S::KS];
-          read_k(ka, buf);
-          f32x16 sc[kNT];
+        for (int t = 0; t < kNT; ++t) sc[t][kh] = f32x16{};
 #pragma unroll
-          for (int t = 0; t < kNT; ++t) sc[t] = f32x16{};
+        for (int s = 0; s < S::KS; ++s)
 #pragma unroll
-          for (int s = 0; s < S::KS; ++s)
+          for (int t = 0; t < kNT; ++t)
+            sc[t][kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[s], qop[t][s], sc[t][kh], 0, 0, 0);
+      }
+      if constexpr (S::V_EARLY) read_v(va[0], buf, 0);   // its latency overlaps the softmax
 #pragma unroll
-            for (int t = 0; t < kNT; ++t) sc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[s], qop[t][s], sc[t], 0, 0, 0);
-          read_v(va, buf);   // independent of the softmax: its latency overlaps it
+      for (int t = 0; t < kNT; ++t) softmax(t, kb, buf, sc[t]);
 #pragma unroll
-          for (int t = 0; t < kNT; ++t) softmax(t, kb, buf, sc[t]);
+      for (int kh = S::V_EARLY ? 1 : 0; kh < kKH; ++kh) read_v(va[kh], buf, kh);
 #pragma unroll
-          for (int s = 0; s < S::KS; ++s)
+      for (int kh = 0; kh < kKH; ++kh)
 #pragma unroll
-            for (int t = 0; t < kNT; ++t)
-              acc[t][s % S::DT] =
-                  __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[s], pb[t][s / S::DT], acc[t][s % S::DT], 0, 0, 0);
+        for (int s = 0; s < S::KS; ++s)
+#pragma unroll
+          for (int t = 0; t < kNT; ++t)
+            acc[t][s % S::DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[kh][s], pb[t][kh][s / S::DT],
+                                                                        acc[t][s % S::DT], 0, 0, 0);
+    }
+  };
+
+  // 3. Key blocks.
+  if constexpr (S::DMA) {
+    // Iteration kb starts the DMA of block kb + 2 into buffer (kb + 2) % 3 (read
+    // last in iteration kb - 1), computes block kb, then waits until only block
+    // kb + 2's DMAs are outstanding (block kb + 1 has landed) before the barrier.
+    // Past the keys the DMAs read nothing, so every iteration issues the same count.
+    constexpr int kDmaPerBlock = S::LPL * kKH;
+    {
+      int pid[kKH];
+      page_ids(0, pid);
+      dma_issue(0, 0, pid);
+      page_ids(1, pid);
+      dma_issue(1, 1, pid);
+    }
+    int pid_next[kKH];
+    page_ids(2, pid_next);
+    dma_barrier<kDmaPerBlock>();
+    for (int kb0 = 0; kb0 < nkb; kb0 += 3) {
+#pragma unroll
+      for (int u = 0; u < 3; ++u) {
+        const int kb = kb0 + u;
+        if (kb < nkb) {
+          dma_issue(kb + 2, (u + 2) % 3, pid_next);
+          compute_block(kb, u);
+          page_ids(kb + 3, pid_next);
+          dma_barrier<kDmaPerBlock>();
         }
-        if (kb + 1 < nkb) stage_write((u + 1) % PD, buf ^ 1);
-        __syncthreads();
+      }
+    }
+    if (bad_pages && lane == 0) atomicOr(p.flags, kFlagBadPage);
+  } else {
+    // Blocks 0 .. PD-1 are loaded before the loop, block 0 is written to LDS, and
+    // iteration kb loads block kb + PD (past the wave's keys nothing is read, but
+    // the loads are issued so that every iteration has the same loads in flight),
+    // computes block kb and writes block kb + 1 to the other buffer.  The loop is
+    // unrolled PD times so that each register set is fixed.
+    {
+      int pid[kKH];
+#pragma unroll
+      for (int u = 0; u < PD; ++u) {
+        page_ids(u, pid);
+        stage_load(u, u, pid);
+      }
+    }
+    int pid_next[kKH];
+    page_ids(PD, pid_next);
+    stage_write(0, 0);
+    __syncthreads();
+    for (int kb0 = 0; kb0 < nkb; kb0 += PD) {
+#pragma unroll
+      for (int u = 0; u < PD; ++u) {
+        const int kb = kb0 + u;
+        if (kb < nkb) {
+          const int buf = kb & 1;
+          stage_load(kb + PD, u, pid_next);
+          compute_block(kb, buf);
+          if (kb + 1 < nkb) stage_write((u + 1) % PD, buf ^ 1);
+          // The next page ids are read here: a scalar load shares its completion
+          // counter with the LDS reads, so issued earlier it would hold up the
+          // first MFMA's operand wait; here the barrier's wait covers it.
+          page_ids(kb + PD + 1, pid_next);
+          __syncthreads();
+        }
       }
     }
   }
