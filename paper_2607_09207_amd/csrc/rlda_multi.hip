@@ -14,10 +14,10 @@
 // which attend to the most keys, are dispatched first.
 //
 // Keys.  The workgroup walks its causal key range in blocks of 32 keys (two
-// pages).  Each wave loads one page of K or V of a block into registers two
-// blocks ahead (page ids come through the scalar cache one block before that) and
-// writes it to LDS (as bf16; fp8 is converted exactly on the way) while the block
-// before it is computed:
+// pages).  Each wave brings one page of K or V of every block, two blocks ahead
+// (page ids come through the scalar cache one block before that): bf16 pages at
+// d = 128 by buffer-load DMA straight into LDS, other caches through registers
+// (fp8 converted exactly to bf16 on the way).  Per block:
 //   S^T[key][row] = K Q^T    v_mfma_f32_32x32x16_bf16, K from LDS, Q in registers;
 //   online softmax per row (lanes l and l^32 hold one row), with the reference
 //   maximum moved only when a score exceeds it by more than 2^8;
