@@ -181,7 +181,7 @@ def multi_bench(args, torch, dev, w, h, ws):
     def call(i, events=None):
         s = sets[i % len(sets)]
         h.multi(s["q"], s["k_cache"], s["v_cache"], s["block_table"], s["seq_lens"], qs, k_scale=s["k_scale"],
-                v_scale=s["v_scale"], out=out, workspace=ws, stream=stream, events=events)
+                v_scale=s["v_scale"], out=out, workspace=ws, stream=stream, events=events, max_q_len=args.max_q_len)
 
     log(f"warmup {args.warmup}")
     for i in range(args.warmup):
@@ -215,7 +215,11 @@ def multi_bench(args, torch, dev, w, h, ws):
         roof = {"bound": "hbm", "achieved": round(nbytes / (kern_ms * 1e-3) / 1e9, 2), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s"}
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = measured_traffic(w.name, MULTI_SOURCES)
+    # max_q_len <= 16 with at most 64 rows per (sequence, KV head): the decode kernel runs the call
+    G = w.num_q_heads // w.num_kv_heads
+    rows_path = 1 <= args.max_q_len <= 16 and args.max_q_len * G <= 64
+    roof["traffic"] = measured_traffic(w.name + ("_rows" if rows_path else ""),
+                                       KERNEL_SOURCES if rows_path else MULTI_SOURCES)
     log(f"ms/step {ms_per_step:.4f}  kernel avg {kern_ms:.4f} ms (p10 {np.percentile(per_call, 10):.4f}, "
         f"p90 {np.percentile(per_call, 90):.4f})  {value:.1f} TFLOP/s  rows/s {rows / (ms_per_step * 1e-3):.0f}")
     result = {
@@ -226,7 +230,8 @@ def multi_bench(args, torch, dev, w, h, ws):
         "config": {"workload": w.name, "batch": w.batch, "query_rows": rows, "num_q_heads": w.num_q_heads,
                    "num_kv_heads": w.num_kv_heads, "head_dim": w.head_dim, "kv_dtype": w.kv_dtype,
                    "sum_seq_lens": int(w.seq_lens.sum()), "flops_per_step": flops, "bytes_per_step": nbytes,
-                   "query_rows_per_s": round(rows / (ms_per_step * 1e-3), 1), "kv_sets_rotated": len(sets)},
+                   "query_rows_per_s": round(rows / (ms_per_step * 1e-3), 1), "kv_sets_rotated": len(sets),
+                   "max_q_len": args.max_q_len, "kernel": "decode page stream" if rows_path else "128-row MFMA"},
         "roofline": roof,
     }
     if args.cpu_budget > 0:
@@ -266,6 +271,8 @@ def main():
                          "(prompt_prefill_grpo_bf16, chunked_prefill_gqa_bf16); "
                          "copy: a plain device copy of --copy-mib MiB, the reference for HBM counter scaling")
     ap.add_argument("--copy-mib", type=int, default=256)
+    ap.add_argument("--max-q-len", type=int, default=0,
+                    help="multi mode: bound on query rows per sequence passed to run_multi (0: none)")
     ap.add_argument("--prompt-tokens", type=int, default=0,
                     help="GRPO workload only: prompt length shared by each group (default 512)")
     ap.add_argument("--grouped", choices=["on", "off"], default="off",

@@ -203,36 +203,46 @@ rlda_status rl_decode_attn_append(rl_decode_attn_t handle, int32_t batch, int32_
                                   size_t workspace_bytes, void* stream);
 
 /*
- * Multi-token queries: attention for prefill chunks (or any query rows that are
- * the last tokens of their sequences).  Rollout prefills the prompt tokens before
- * decoding (Sec. 3; the prefill cost of App. A.1.2, whose attention term grows with
- * the square of the prompt length).  Sequence b has n_b = q_start[b+1] - q_start[b]
- * query rows q[q_start[b] + i], 0 <= i < n_b: its last n_b cached tokens (their K/V
- * already in the cache, e.g. written by a prefill pass), so row i is at position
- * seq_lens[b] - n_b + i and attends causally to positions 0 .. seq_lens[b] - n_b + i:
+ * Multi-token queries: attention for prefill chunks, or for verifying a few
+ * drafted tokens (any query rows that are the last tokens of their sequences).
+ * Rollout prefills the prompt tokens before decoding (Sec. 3; the prefill cost of
+ * App. A.1.2, whose attention term grows with the square of the prompt length).
+ * Sequence b has n_b = q_start[b+1] - q_start[b] query rows q[q_start[b] + i],
+ * 0 <= i < n_b: its last n_b cached tokens (their K/V already in the cache), so
+ * row i is at position seq_lens[b] - n_b + i and attends causally to positions
+ * 0 .. seq_lens[b] - n_b + i:
  *   out[q_start[b] + i][h] = sum_{t <= pos} softmax_t(scale * q[.][h] . k_t) v_t.
  * n_b = 1 for every sequence is rl_decode_attn_run (up to rounding order).
  *   q            [total_q][Hq][d]   q_dtype (bf16)
  *   q_start      [batch + 1] int32, device memory, 0 <= q_start[b] <= q_start[b+1] <= total_q
  *   out          [total_q][Hq][d]   out_dtype; rows no sequence names are not written
  *   total_q      host value: rows of q and out
- *   other arrays and `workspace` as for rl_decode_attn_run (only its flag word is used).
- * The (token, head) pairs of one (sequence, KV head) are processed 128 at a time by
- * one workgroup, as 32x32 MFMA tiles (bf16 products, fp32 accumulation), so each
- * K/V page is read once per 128 query rows.  Supported for bf16 and fp8 caches
- * and batch <= 4096 (RLDA_ERR_UNSUPPORTED for f32, a larger batch, or q of 2^31
- * bytes or more).
- * Device-side checks: a sequence with inconsistent q_start entries gets no rows
- * (flag bit 1); n_b > seq_lens[b] raises flag bit 1 and rows at negative positions
- * are zero; lengths beyond capacity and out-of-pool pages as for rl_decode_attn_run.
- * One kernel, asynchronous; event_begin / event_end (hipEvent_t): both NULL, or
- * both given to be recorded around it.
+ *   max_q_len    host value, 0 or an upper bound on every n_b.  When
+ *                1 <= max_q_len <= 16 and max_q_len * G <= 64 (and batch * Hkv *
+ *                max_pages_per_seq * ceil(max_q_len * G / 16) < 2^31), the call runs
+ *                on the decode kernel's page stream (the n_b * G rows of each
+ *                (sequence, KV head) as up to four 16-row MFMA tiles, each streaming
+ *                the pages, long sequences split across workgroups; workspace as
+ *                for rl_decode_attn_run, counters included); a sequence with
+ *                n_b > max_q_len then gets no rows and raises flag bit 1.  Otherwise
+ *                the (token, head) pairs of one (sequence, KV head) are processed 128
+ *                at a time by one workgroup as 32x32 MFMA tiles (each K/V page read
+ *                once per 128 rows), batch <= 4096, and only the flag word of the
+ *                workspace is used.
+ *   other arrays and `workspace` as for rl_decode_attn_run.
+ * Supported for bf16 and fp8 caches (RLDA_ERR_UNSUPPORTED for f32, and when q
+ * holds 2^31 bytes or more).  Device-side checks: a sequence with inconsistent
+ * q_start entries gets no rows (flag bit 1); n_b > seq_lens[b] raises flag bit 1
+ * and rows at negative positions are zero; lengths beyond capacity and
+ * out-of-pool pages as for rl_decode_attn_run.  One kernel, asynchronous;
+ * event_begin / event_end (hipEvent_t): both NULL, or both given to be recorded
+ * around it.
  */
 rlda_status rl_decode_attn_run_multi(rl_decode_attn_t handle, int32_t batch, int32_t num_pages, int32_t total_q,
-                                     const void* q, const void* k_cache, const void* v_cache, const float* k_scale,
-                                     const float* v_scale, const int32_t* block_table, const int32_t* seq_lens,
-                                     const int32_t* q_start, void* out, void* workspace, size_t workspace_bytes,
-                                     void* stream, void* event_begin, void* event_end);
+                                     int32_t max_q_len, const void* q, const void* k_cache, const void* v_cache,
+                                     const float* k_scale, const float* v_scale, const int32_t* block_table,
+                                     const int32_t* seq_lens, const int32_t* q_start, void* out, void* workspace,
+                                     size_t workspace_bytes, void* stream, void* event_begin, void* event_end);
 
 /* Flags raised by device-side contract checks since the workspace was zeroed
  * (bit 0: page id outside [0, num_pages); bit 1: seq_len beyond capacity;

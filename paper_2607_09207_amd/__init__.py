@@ -140,10 +140,12 @@ class DecodeAttention:
         return out
 
     def multi(self, q, k_cache, v_cache, block_table, seq_lens, q_start, k_scale=None, v_scale=None, out=None,
-              workspace=None, stream=None, num_pages: Optional[int] = None, events=None):
+              workspace=None, stream=None, num_pages: Optional[int] = None, events=None, max_q_len: int = 0):
         """Multi-token queries (rl_decode_attn_run_multi): q [total_q][Hq][d], q_start
         [batch + 1] int32 device tensor; sequence b's rows q[q_start[b]:q_start[b+1]]
-        are its last tokens and attend causally.  Returns out [total_q][Hq][d]."""
+        are its last tokens and attend causally.  max_q_len (host value) bounds the
+        rows per sequence; with max_q_len * G <= 16 the decode kernel's page stream
+        runs the call.  Returns out [total_q][Hq][d]."""
         torch = _torch()
         total = int(q.shape[0])
         B = int(q_start.shape[0]) - 1
@@ -160,7 +162,8 @@ class DecodeAttention:
         ptr = lambda t: None if t is None else t.data_ptr()
         wp = self._aligned_ptr(ws)
         e0, e1 = (None, None) if events is None else tuple(self._event_handle(e) for e in events)
-        _abi.check(self._lib.rl_decode_attn_run_multi(self._h, B, npages, total, ptr(q), ptr(k_cache), ptr(v_cache),
+        _abi.check(self._lib.rl_decode_attn_run_multi(self._h, B, npages, total, int(max_q_len), ptr(q), ptr(k_cache),
+                                                      ptr(v_cache),
                                                       ptr(k_scale), ptr(v_scale), ptr(block_table), ptr(seq_lens),
                                                       ptr(q_start), ptr(out), wp, ws.numel() - (wp - ws.data_ptr()),
                                                       stream, e0, e1),

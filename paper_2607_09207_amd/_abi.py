@@ -69,7 +69,7 @@ def load() -> ctypes.CDLL:
         lib.rl_decode_attn_grouped_workspace_size.restype = ctypes.c_int
         lib.rl_decode_attn_append.argtypes = [vp, i32, i32] + [vp] * 8 + [vp, sz, vp]
         lib.rl_decode_attn_append.restype = ctypes.c_int
-        lib.rl_decode_attn_run_multi.argtypes = [vp, i32, i32, i32] + [vp] * 9 + [vp, sz, vp, vp, vp]
+        lib.rl_decode_attn_run_multi.argtypes = [vp, i32, i32, i32, i32] + [vp] * 9 + [vp, sz, vp, vp, vp]
         lib.rl_decode_attn_run_multi.restype = ctypes.c_int
         lib.rl_decode_attn_read_flags.argtypes = [vp, vp, vp, ctypes.POINTER(ctypes.c_uint32)]
         lib.rl_decode_attn_read_flags.restype = ctypes.c_int

@@ -6,6 +6,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <new>
 
@@ -41,9 +42,13 @@ WsLayout layout_of(const rlda_handle* h) {
   WsLayout w;
   w.flags = 0;
   w.counters = align_up(sizeof(uint32_t));
-  w.part_ml = align_up(w.counters + sizeof(uint32_t) * (size_t)c.max_batch * c.num_kv_heads);
-  w.part_acc = align_up(w.part_ml + sizeof(float) * 2 * (size_t)h->ws_ranges * h->group * 2);
-  w.total = align_up(w.part_acc + sizeof(float) * 2 * (size_t)h->ws_ranges * h->group * c.head_dim);
+  // Counters: one per (sequence, KV head) segment, or per 16-row chunk of one in
+  // multi-token runs through the decode kernel.
+  w.part_ml = align_up(w.counters + sizeof(uint32_t) * (size_t)c.max_batch * c.num_kv_heads * rlda::kMaxRowChunks);
+  // Partial slots: two per work range, 16 rows each (G rows in decode runs, up to
+  // 16 rows of a segment in multi-token runs).
+  w.part_acc = align_up(w.part_ml + sizeof(float) * 2 * (size_t)h->ws_ranges * rlda::kMaxGroup * 2);
+  w.total = align_up(w.part_acc + sizeof(float) * 2 * (size_t)h->ws_ranges * rlda::kMaxGroup * c.head_dim);
   w.gprefix = w.total;
   w.pfx_ml = align_up(w.gprefix + sizeof(int32_t) * (size_t)c.max_batch);
   w.pfx_acc = align_up(w.pfx_ml + sizeof(float) * 2 * (size_t)c.max_batch * c.num_q_heads);
@@ -214,6 +219,7 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32
   p.counters = (uint32_t*)(ws + wl.counters);
   p.part_ml = (float*)(ws + wl.part_ml);
   p.part_acc = (float*)(ws + wl.part_acc);
+  p.part_rows = h->group;
   const int eb = elem_bytes(c.kv_dtype);
   p.stride_page = h->stride_page * eb;
   p.stride_head = h->stride_head * eb;
@@ -246,7 +252,7 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32
   if (jobs * rlda::kMaxRanges > INT32_MAX) return RLDA_ERR_UNSUPPORTED;
   // Split each job over several workgroups until the prompt pass fills the CUs,
   // within the partial-slot capacity the workspace has (64-row slots).
-  const int64_t slots = 2 * (int64_t)h->ws_ranges * h->group / 64;
+  const int64_t slots = 2 * (int64_t)h->ws_ranges * rlda::kMaxGroup / 64;
   int64_t split = jobs >= ranges ? 1 : ranges / jobs;
   if (split > 8) split = 8;
   if (split * jobs > slots) split = slots / jobs;
@@ -336,16 +342,23 @@ rlda_status rl_decode_attn_append(rl_decode_attn_t h, int32_t batch, int32_t num
 }
 
 rlda_status rl_decode_attn_run_multi(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32_t total_q,
-                                     const void* q, const void* k_cache, const void* v_cache, const float* k_scale,
-                                     const float* v_scale, const int32_t* block_table, const int32_t* seq_lens,
-                                     const int32_t* q_start, void* out, void* workspace, size_t workspace_bytes,
-                                     void* stream, void* event_begin, void* event_end) {
+                                     int32_t max_q_len, const void* q, const void* k_cache, const void* v_cache,
+                                     const float* k_scale, const float* v_scale, const int32_t* block_table,
+                                     const int32_t* seq_lens, const int32_t* q_start, void* out, void* workspace,
+                                     size_t workspace_bytes, void* stream, void* event_begin, void* event_end) {
   if (!h) return RLDA_ERR_INVALID_ARG;
   const rl_decode_attn_config& c = h->cfg;
-  if (batch < 0 || batch > c.max_batch || num_pages < 0 || total_q < 0) return RLDA_ERR_INVALID_ARG;
+  if (batch < 0 || batch > c.max_batch || num_pages < 0 || total_q < 0 || max_q_len < 0) return RLDA_ERR_INVALID_ARG;
   if ((!event_begin) != (!event_end)) return RLDA_ERR_INVALID_ARG;
-  if (h->kind == rlda::KvKind::F32 || batch > rlda::kMultiMaxBatch) return RLDA_ERR_UNSUPPORTED;
-  // The kernel addresses q with 32-bit byte offsets.
+  if (h->kind == rlda::KvKind::F32) return RLDA_ERR_UNSUPPORTED;
+  // Few rows per sequence: the decode kernel's page stream, which splits long
+  // sequences across workgroups, each (sequence, KV head) as up to 4 segments of
+  // 16 rows.  Otherwise the 128-row MFMA kernel.
+  const int64_t row_chunks = ((int64_t)max_q_len * h->group + rlda::kMaxGroup - 1) / rlda::kMaxGroup;
+  const bool rows_path = max_q_len >= 1 && max_q_len <= rlda::kMaxRowsQLen && row_chunks <= rlda::kMaxRowChunks &&
+                         (int64_t)batch * c.max_pages_per_seq * c.num_kv_heads * row_chunks <= INT32_MAX;
+  if (!rows_path && batch > rlda::kMultiMaxBatch) return RLDA_ERR_UNSUPPORTED;
+  // The kernels address q with 32-bit byte offsets.
   if ((int64_t)total_q * c.num_q_heads * c.head_dim * 2 > INT32_MAX) return RLDA_ERR_UNSUPPORTED;
   if (batch == 0 || total_q == 0) return RLDA_OK;
   if (!q || !block_table || !seq_lens || !q_start || !out) return RLDA_ERR_INVALID_ARG;
@@ -359,11 +372,7 @@ rlda_status rl_decode_attn_run_multi(rl_decode_attn_t h, int32_t batch, int32_t 
   const WsLayout wl = layout_of(h);
   if (!workspace || ((uintptr_t)workspace % kAlign)) return RLDA_ERR_WORKSPACE;
   if (workspace_bytes < wl.total) return RLDA_ERR_WORKSPACE;
-  // One workgroup per (128-row block, KV head): a sequence's n_b * G rows take at
-  // most n_b * G / 128 + 1 blocks, so this grid covers every consistent q_start.
-  const int64_t blocks = ((int64_t)total_q * h->group + rlda::kMultiRows - 1) / rlda::kMultiRows + batch;
-  const int64_t grid = blocks * c.num_kv_heads;
-  if (grid > INT32_MAX) return RLDA_ERR_UNSUPPORTED;
+  char* ws = (char*)workspace;
   rlda::Params p;
   memset(&p, 0, sizeof p);
   p.q = q;
@@ -375,8 +384,9 @@ rlda_status rl_decode_attn_run_multi(rl_decode_attn_t h, int32_t batch, int32_t 
   p.seq_lens = seq_lens;
   p.q_start = q_start;
   p.total_q = total_q;
+  p.max_q_len = max_q_len;
   p.out = out;
-  p.flags = (uint32_t*)((char*)workspace + wl.flags);
+  p.flags = (uint32_t*)(ws + wl.flags);
   const int eb = elem_bytes(c.kv_dtype);
   p.stride_page = h->stride_page * eb;
   p.stride_head = h->stride_head * eb;
@@ -390,6 +400,32 @@ rlda_status rl_decode_attn_run_multi(rl_decode_attn_t h, int32_t batch, int32_t 
   p.scale_log2 = h->scale * 1.4426950408889634f;
   p.out_bf16 = c.out_dtype == RLDA_BF16;
   memcpy(p.q_head, h->q_head, sizeof p.q_head);
+  if (rows_path) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return RLDA_ERR_HIP;
+    int ranges = c.num_work_ranges > 0 ? c.num_work_ranges : cu_count(dev);
+    if (ranges <= 0) return RLDA_ERR_HIP;
+    // Partial slots hold one segment's rows (at most 16) each.
+    p.row_chunks = (int)row_chunks;
+    p.part_rows = std::min<int>(max_q_len * h->group, rlda::kMaxGroup);
+    if (ranges > h->ws_ranges) ranges = h->ws_ranges;
+    if (ranges > rlda::kMaxRanges) ranges = rlda::kMaxRanges;
+    const int64_t max_units = (int64_t)batch * c.num_kv_heads * row_chunks * c.max_pages_per_seq;
+    if (ranges > max_units) ranges = (int)max_units;
+    if (ranges < 1) ranges = 1;
+    p.nranges = ranges;
+    p.counters = (uint32_t*)(ws + wl.counters);
+    p.part_ml = (float*)(ws + wl.part_ml);
+    p.part_acc = (float*)(ws + wl.part_acc);
+    if (rlda::launch_decode_rows(h->kind, c.head_dim, p, stream, event_begin, event_end) != hipSuccess)
+      return RLDA_ERR_HIP;
+    return RLDA_OK;
+  }
+  // One workgroup per (row block, KV head): a sequence's n_b * G rows take at most
+  // n_b * G / rows_per_block + 1 blocks, so this grid covers every consistent q_start.
+  const int64_t blocks = ((int64_t)total_q * h->group + rlda::kMultiRows - 1) / rlda::kMultiRows + batch;
+  const int64_t grid = blocks * c.num_kv_heads;
+  if (grid > INT32_MAX) return RLDA_ERR_UNSUPPORTED;
   if (rlda::launch_multi(h->kind, c.head_dim, p, (int)grid, stream, event_begin, event_end) != hipSuccess)
     return RLDA_ERR_HIP;
   return RLDA_OK;

@@ -127,8 +127,9 @@ __device__ __forceinline__ void store_out(const Params& p, int b, int qh, int d0
 __shared__ int16_t s_qhead[kMaxQHeads];
 
 // Partials of split segments live in the workspace: slot sl of query row h holds
-// (m, l) at part_ml[(sl*G + h)*2] and the unnormalised output at
-// part_acc[(sl*G + h)*D ...], sl < 2*nranges.  They are written and read with the
+// (m, l) at part_ml[(sl*R + h)*2] and the unnormalised output at
+// part_acc[(sl*R + h)*D ...], sl < 2*nranges, R = part_rows (G, or the rows of a
+// multi-token segment).  They are written and read with the
 // sc1 cache policy (device scope: write-through past the XCD's L2 and read from
 // the coherent level), so workgroups on different XCDs exchange them without L2
 // writeback or invalidate.
@@ -137,7 +138,7 @@ struct PartialRsrc {
   __amdgpu_buffer_rsrc_t acc, ml;
   template <int D>
   __device__ __forceinline__ static PartialRsrc of(const Params& p) {
-    const uint32_t slots = 2u * (uint32_t)p.nranges * (uint32_t)p.group;
+    const uint32_t slots = 2u * (uint32_t)p.nranges * (uint32_t)p.part_rows;
     return {make_rsrc_uni(p.part_acc, slots * D * 4u), make_rsrc_uni(p.part_ml, slots * 8u)};
   }
 };
@@ -162,7 +163,7 @@ template <int D, int kBatch>
 __device__ __forceinline__ void merge_batches(const Params& p, const PartialRsrc& rs, int h, int d0, int64_t u_first,
                                               int64_t u_last, float& M, float& Ls, float* o) {
   constexpr int DPT = D / 16;
-  const int G = p.group;
+  const int G = p.part_rows;
   for (int64_t k0 = u_first; k0 <= u_last; k0 += kBatch) {
     u32x2 ml[kBatch];
     float v[kBatch][DPT];
@@ -186,7 +187,7 @@ __device__ __forceinline__ void merge_batches(const Params& p, const PartialRsrc
 // A segment cut into many pieces (a long sequence over few workgroups' worth of
 // other work) is merged 16 pieces per round trip; the common 2-4 pieces, 4 at a time.
 template <int D>
-__device__ __forceinline__ void merge_pieces(const Params& p, int b, int g, int h, int d0, int64_t u_first,
+__device__ __forceinline__ void merge_pieces(const Params& p, int orow, int qh, int h, int d0, int64_t u_first,
                                              int64_t u_last) {
   constexpr int DPT = D / 16;
   const PartialRsrc rs = PartialRsrc::of<D>(p);
@@ -197,7 +198,7 @@ __device__ __forceinline__ void merge_pieces(const Params& p, int b, int g, int 
     merge_batches<D, 16>(p, rs, h, d0, u_first, u_last, M, Ls, o);
   else
     merge_batches<D, 4>(p, rs, h, d0, u_first, u_last, M, Ls, o);
-  store_out<D>(p, b, s_qhead[g * p.group + h], d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
+  store_out<D>(p, orow, qh, d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
 }
 
 // ---------------------------------------------------------------- MFMA policy
@@ -236,6 +237,9 @@ struct Mfma {
   float m, l;
   QOp q;
   int koff[KL], voff[4], qoff[KS];
+  // Multi-token rows: how many tokens this lane's row sits before its segment's
+  // last query token (keys at or past valid_tokens - shift of a page are masked).
+  int shift = 0;
 
   __device__ __forceinline__ static int chunk_of(int qg, int s) {
     return FP8 ? 8 * (s >> 1) + 2 * qg + (s & 1) : 4 * s + qg;
@@ -261,6 +265,21 @@ struct Mfma {
     const uint16_t* qb = (const uint16_t*)p.q + (int64_t)b * p.num_q_heads * D;
     const __amdgpu_buffer_rsrc_t r = make_rsrc_uni(qb, load ? (uint32_t)(p.num_q_heads * D * 2) : 0u);
     const int row = (i < G) ? s_qhead[g * G + i] * D * 2 : kPastRange;
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      qo.v[s] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, row + 16 * chunk_of(qg, s), 0, 0));
+  }
+
+  // Q operand of a multi-token segment: tile row i is row rr = r0 + i of the
+  // (sequence, KV head), query head (rr % G) of query row q0 + rr / G; rows at or
+  // past n * G read zeros.
+  __device__ __forceinline__ static void load_q_multi(QOp& qo, const Params& p, int q0, int n, int g, int r0, int lane,
+                                                      bool load) {
+    if (!load) return;
+    const int i = lane & 15, qg = lane >> 4, G = p.group, rr = r0 + i;
+    const __amdgpu_buffer_rsrc_t r =
+        make_rsrc_uni(p.q, (uint32_t)p.total_q * (uint32_t)p.num_q_heads * D * 2u);
+    const int row = (rr < n * G) ? ((q0 + rr / G) * p.num_q_heads + s_qhead[g * G + rr % G]) * D * 2 : kPastRange;
 #pragma unroll
     for (int s = 0; s < KS; ++s)
       qo.v[s] = __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, row + 16 * chunk_of(qg, s), 0, 0));
@@ -352,7 +371,9 @@ struct Mfma {
     }
   }
 
-  // Page with index `j` in its sequence; `valid_tokens` tokens of it count.
+  // Page with index `j` in its sequence; `valid_tokens` tokens of it count (for
+  // multi-token rows: tokens of the page and after it, up to 31, less `shift`).
+  template <bool MULTI = false>
   __device__ __forceinline__ void compute(const Frag& f, int lane, int valid_tokens, float kmul, float vmul) {
     const int qg = lane >> 4;
     f32x4 sc = {0.f, 0.f, 0.f, 0.f};
@@ -360,9 +381,10 @@ struct Mfma {
     for (int s = 0; s < KS; ++s) sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k_operand(f, s), q.v[s], sc, 0, 0, 0);
     float sv[4];
     float mx = neg_inf();
+    const int vt = MULTI ? valid_tokens - shift : valid_tokens;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      sv[r] = (4 * qg + r < valid_tokens) ? sc[r] * kmul : neg_inf();
+      sv[r] = (4 * qg + r < vt) ? sc[r] * kmul : neg_inf();
       mx = fmaxf(mx, sv[r]);
     }
     mx = group_max(mx);
@@ -373,8 +395,11 @@ struct Mfma {
     const bool up = mx > m + kRescaleLog2;   // always when m is still -inf and mx is not
     if (__builtin_amdgcn_ballot_w64(up) != 0)
     {
+      // Multi-token rows: a row whose keys are all masked so far keeps m = -inf
+      // while other rows move, so alpha comes from `up` (1 otherwise).
       const float mn = up ? mx : m;
-      const float alpha = __builtin_amdgcn_exp2f(m - mn);   // 0 from -inf, 1 when unchanged
+      const float alpha = MULTI ? (up ? __builtin_amdgcn_exp2f(m - mx) : 1.f)
+                                : __builtin_amdgcn_exp2f(m - mn);   // 0 from -inf, 1 when unchanged
       l *= alpha;
       m = mn;
 #pragma unroll
@@ -437,6 +462,20 @@ struct Mfma {
       sml[i][0] = m;
       sml[i][1] = lt;
     }
+  }
+
+  // A multi-token segment this wave covered entirely: tile row i is row
+  // rr = r0 + i < n * G, output row q0 + rr / G, query head (rr % G) of KV head g.
+  __device__ __forceinline__ void write_out_multi(const Params& p, int q0, int n, int g, int r0, int lane) const {
+    const int i = lane & 15, qg = lane >> 4, G = p.group, rr = r0 + i;
+    const float lt = group_sum(l);
+    if (rr >= n * G) return;
+    float o[4 * DT];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int t = 0; t < DT; ++t) o[r * DT + t] = acc[t][r];
+    store_row<D, 4 * DT>(p, q0 + rr / G, s_qhead[g * G + rr % G], 4 * DT * qg, o, lt > 0.f ? 1.f / lt : 0.f);
   }
 
   // A piece this wave covered entirely: normalise and write its rows.
@@ -590,6 +629,7 @@ constexpr int kInfoEnd = 1 << 8;        // last position of this wave's quarter
 constexpr int kInfoHeadShift = 9;       // KV head g: 8 bits
 constexpr int kInfoSeqShift = 17;       // sequence b: 13 bits (b < 8192)
 constexpr int kInfoPrompt = 1 << 30;    // grouped run: the sequence's prompt pass state seeds its first page
+constexpr int kInfoChunkShift = 30;     // multi-token run: the segment's 16-row chunk (2 bits)
 
 // The page id is returned as read; it is checked where it is used, so that
 // nothing waits for these loads until the chunk is consumed.
@@ -598,42 +638,56 @@ struct StreamChunk {
   int info;     // bits above
 };
 
-// Positions fit in 32 bits: the host rejects max_batch * max_pages * Hkv >= 2^31.
+// Positions fit in 32 bits: the host rejects max_batch * max_pages * Hkv (times
+// the row chunks of a multi-token run) >= 2^31.
+// Multi-token runs report, instead of a page's valid tokens, the tokens from the
+// page's start to the sequence's end (up to 31), which the rows' causal masks
+// need, and split a (sequence, KV head) with more than 16 rows into nrc segments
+// of 16 rows that each stream the pages: segment gv = g * nrc + rc of a sequence,
+// Hs = Hkv * nrc segments per sequence.
+template <bool MULTI>
 __device__ __forceinline__ StreamChunk fetch_chunk(const Params& p, const int32_t* s_pre, const uint8_t* s_tail,
-                                                   const int32_t* s_ppre, int base, int w0, int w1, int lane) {
+                                                   const int32_t* s_ppre, int base, int w0, int w1, int lane, int Hs,
+                                                   int nrc) {
   StreamChunk c = {-1, 0};
   const int pos = base + lane;
   if (pos < w1) {
-    const int Hkv = p.num_kv_heads;
-    const int y = (int)((uint32_t)pos / (uint32_t)Hkv);
+    const int y = (int)((uint32_t)pos / (uint32_t)Hs);
     int lo = 0, hi = p.batch;   // s_pre[lo] <= y < s_pre[hi]
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
       if (s_pre[mid] <= y) lo = mid; else hi = mid;
     }
     const int b = lo, pre = s_pre[b], nb = s_pre[b + 1] - pre;
-    const int off = pos - Hkv * pre;
-    const int g = (int)((uint32_t)off / (uint32_t)nb), j = off - g * nb;
-    const int tok = (j == nb - 1) ? s_tail[b] : kPage;
-    const int pp = s_ppre[b];   // prompt pages handled by the prompt pass (grouped runs)
+    const int off = pos - Hs * pre;
+    const int gv = (int)((uint32_t)off / (uint32_t)nb), j = off - gv * nb;
+    const int g = MULTI ? (int)((uint32_t)gv / (uint32_t)nrc) : gv;
+    const int tok = (j == nb - 1) ? s_tail[b] : (MULTI ? (j == nb - 2 ? min(kPage + s_tail[b], 31) : 31) : kPage);
+    const int pp = MULTI ? 0 : s_ppre[b];   // prompt pages handled by the prompt pass (grouped runs)
     c.pid = p.block_table[(int64_t)b * p.max_pages + pp + j];
     c.info = tok | (j == 0 ? kInfoFirst : 0) | (j == nb - 1 ? kInfoLast : 0) | (pos == w0 ? kInfoStart : 0) |
              (pos == w1 - 1 ? kInfoEnd : 0) | (g << kInfoHeadShift) | (b << kInfoSeqShift) |
-             (pp > 0 ? kInfoPrompt : 0);
+             (MULTI ? (gv - g * nrc) << kInfoChunkShift : (pp > 0 ? kInfoPrompt : 0));
   }
   return c;
 }
 
 // ---------------------------------------------------------------- the kernel
 
-template <class Pol>
+// MULTI: multi-token rows (rl_decode_attn_run_multi with at most 16 * row_chunks
+// rows per (sequence, KV head)): (b, g) has n_b * G rows, row r is query head
+// (r % G) of query row q_start[b] + r / G and sees keys below L - n_b + r / G + 1;
+// its rows are streamed as row_chunks segments of 16 rows each.
+template <class Pol, bool MULTI = false>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(1, 1)))
 void decode_attention_kernel(const Params p) {
   constexpr int D = Pol::kD;
   constexpr int DPT = D / 16;   // output elements per thread in the workgroup merge
   __shared__ int32_t s_pre[kMaxBatch + 1];
   __shared__ uint8_t s_tail[kMaxBatch];   // valid tokens of each sequence's last page
-  __shared__ int32_t s_ppre[kMaxBatch];   // grouped runs: leading pages covered by the prompt pass
+  // Grouped runs: leading pages covered by the prompt pass.  Multi-token runs:
+  // (q_start[b] << 5) | n_b.
+  __shared__ int32_t s_ppre[kMaxBatch];
   // Cut pieces: slot 2w holds wave w's piece that began before its quarter of the
   // share, slot 2w+1 its piece that continues past it.
   __shared__ __align__(16) float s_acc[2 * kWaves][16][D + 4];
@@ -654,6 +708,8 @@ void decode_attention_kernel(const Params p) {
   }();
   const int batch = p.batch, Hkv = p.num_kv_heads, G = p.group;
   const int cap = p.max_pages * kPage;
+  // Multi-token runs: nrc 16-row segments per (sequence, KV head), Hs per sequence.
+  const int nrc = MULTI ? p.row_chunks : 1, Hs = Hkv * nrc;
 
   // 1. Page counts per sequence and their prefix sums (identical in every workgroup).
   {
@@ -664,12 +720,27 @@ void decode_attention_kernel(const Params p) {
       int L = p.seq_lens[b];
       if (L < 0 || L > cap) bad = 1;
       L = min(max(L, 0), cap);
-      const int nfull = (L + kPage - 1) / kPage;
-      // Grouped runs: the prompt pass covered the first pp pages (its clamp keeps
-      // pp <= floor(L / 16)); this kernel streams the rest.
-      const int pp = p.group_size > 0 ? min(max(p.gprefix[b / p.group_size], 0), L / kPage) : 0;
+      int nfull = (L + kPage - 1) / kPage;
+      int pp = 0;
+      if constexpr (MULTI) {
+        // Inconsistent offsets, or more rows than the call allows: no rows.  More
+        // rows than tokens: flagged; rows before position 0 see no key (zeros).
+        const int q0 = p.q_start[b], q1 = p.q_start[b + 1];
+        int nq = q1 - q0;
+        if (q0 < 0 || q1 < q0 || q1 > p.total_q || nq > p.max_q_len) {
+          bad = 1;
+          nq = 0;
+        }
+        if (nq > L) bad = 1;
+        if (nq == 0) nfull = 0;
+        s_ppre[b] = nq > 0 ? (q0 << 5) | nq : 0;
+      } else {
+        // Grouped runs: the prompt pass covered the first pp pages (its clamp keeps
+        // pp <= floor(L / 16)); this kernel streams the rest.
+        pp = p.group_size > 0 ? min(max(p.gprefix[b / p.group_size], 0), L / kPage) : 0;
+        s_ppre[b] = pp;
+      }
       const int n = nfull - pp;
-      s_ppre[b] = pp;
       s_pre[b + 1] = n;
       s_tail[b] = (uint8_t)(L - (nfull - 1) * kPage);   // 1..16 when nfull > 0
       sum += n;
@@ -694,12 +765,25 @@ void decode_attention_kernel(const Params p) {
     if (tid == 0) s_pre[0] = 0;
     __syncthreads();
   }
-  const int64_t T = uni64((int64_t)s_pre[batch] * Hkv);
+  const int64_t T = uni64((int64_t)s_pre[batch] * Hs);
 
   // 2. Sequences with no pages left to stream: zero rows, or (grouped runs) the
   //    normalised prompt-pass result when the prompt is the whole sequence.
   for (int b = u; b < batch; b += W) {
     if (s_pre[b + 1] != s_pre[b]) continue;
+    if constexpr (MULTI) {
+      // Rows of a sequence with no keys (none, or rows claimed past an empty cache).
+      const int nq = s_ppre[b] & 31, q0 = s_ppre[b] >> 5;
+      const int n = nq * p.num_q_heads * D;
+      for (int e = tid; e < n; e += kThreads) {
+        const int64_t idx = (int64_t)q0 * p.num_q_heads * D + e;
+        if (p.out_bf16)
+          ((uint16_t*)p.out)[idx] = 0;
+        else
+          ((float*)p.out)[idx] = 0.f;
+      }
+      continue;
+    }
     const int n = p.num_q_heads * D;
     const bool prompt = s_ppre[b] > 0;
     for (int e = tid; e < n; e += kThreads) {
@@ -733,11 +817,11 @@ void decode_attention_kernel(const Params p) {
     typename Pol::QOp qring[kDepth];
     typename Pol::PInit pring[kDepth];
     bool began = false;   // the segment being accumulated began inside this quarter
-    StreamChunk nxt = fetch_chunk(p, s_pre, s_tail, s_ppre, w0, w0, w1, lane);
+    StreamChunk nxt = fetch_chunk<MULTI>(p, s_pre, s_tail, s_ppre, w0, w0, w1, lane, Hs, nrc);
     for (int base = w0; base < w1; base += kChunk) {
       const StreamChunk cur = nxt;
       const int cn = min(kChunk, w1 - base);
-      if (base + kChunk < w1) nxt = fetch_chunk(p, s_pre, s_tail, s_ppre, base + kChunk, w0, w1, lane);
+      if (base + kChunk < w1) nxt = fetch_chunk<MULTI>(p, s_pre, s_tail, s_ppre, base + kChunk, w0, w1, lane, Hs, nrc);
       typename Pol::Frag fr[kDepth];
       int sinfo[kDepth];
       float skm[kDepth], svm[kDepth];
@@ -765,9 +849,14 @@ void decode_attention_kernel(const Params p) {
           vs = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(make_rsrc_uni(p.v_scale + si, sb), 0, 0, 0));
         }
         const int64_t po = (pk >= 0) ? (int64_t)pk * p.stride_page + (int64_t)g * p.stride_head : 0;
-        const uint32_t nrec = tok > 0 ? (uint32_t)((tok - 1) * p.stride_slot + D * Pol::kEB) : 0u;
+        const int ptok = MULTI ? min(tok, kPage) : tok;   // tokens of this page
+        const uint32_t nrec = ptok > 0 ? (uint32_t)((ptok - 1) * p.stride_slot + D * Pol::kEB) : 0u;
         st.issue(f, make_rsrc_uni((const char*)p.k + po, nrec), make_rsrc_uni((const char*)p.v + po, nrec));
-        if constexpr (Pol::kQRing) {
+        if constexpr (MULTI) {
+          const int qs = s_ppre[b];
+          Pol::load_q_multi(q_out, p, qs >> 5, qs & 31, g, kPage * ((info >> kInfoChunkShift) & 3), lane,
+                            (info & (kInfoFirst | kInfoStart)) != 0);
+        } else if constexpr (Pol::kQRing) {
           Pol::load_q(q_out, p, b, g, lane, (info & (kInfoFirst | kInfoStart)) != 0);
           Pol::load_prompt(pi_out, p, b, g, lane, (info & kInfoFirst) && (info & kInfoPrompt));
         }
@@ -782,24 +871,34 @@ void decode_attention_kernel(const Params p) {
         const int g = (info >> kInfoHeadShift) & 255, b = (info >> kInfoSeqShift) & 8191;
         if (info & (kInfoFirst | kInfoStart)) {
           bool seeded = false;
-          if constexpr (Pol::kQRing) {
+          if constexpr (Pol::kQRing && !MULTI) {
             if ((info & kInfoFirst) && (info & kInfoPrompt)) {
               st.begin_prompt(q, pi, G, lane);
               seeded = true;
             }
           }
           if (!seeded) st.begin(q, p, b, g, lane);
+          if constexpr (MULTI) {
+            const int nq = s_ppre[b] & 31, r = kPage * ((info >> kInfoChunkShift) & 3) + (lane & 15);
+            st.shift = (r < nq * G) ? nq - 1 - r / G : 0;
+          }
           began = (info & kInfoFirst) != 0;
         }
-        st.compute(f, lane, info & kInfoTok, p.scale_log2 * km, vm);
+        if constexpr (MULTI)
+          st.template compute<true>(f, lane, info & kInfoTok, p.scale_log2 * km, vm);
+        else
+          st.compute(f, lane, info & kInfoTok, p.scale_log2 * km, vm);
         if (info & (kInfoLast | kInfoEnd)) {
           const bool ended = (info & kInfoLast) != 0;
           if (began && ended) {
-            st.write_out(p, b, g, lane);
+            if constexpr (MULTI)
+              st.write_out_multi(p, s_ppre[b] >> 5, s_ppre[b] & 31, g, kPage * ((info >> kInfoChunkShift) & 3), lane);
+            else
+              st.write_out(p, b, g, lane);
           } else {
             const int slot = 2 * wave + (ended ? 0 : 1);
             st.to_lds(s_acc[slot], s_ml[slot], lane);
-            if (lane == 0) s_seg[slot] = b * Hkv + g;
+            if (lane == 0) s_seg[slot] = b * Hs + (MULTI ? g * nrc + ((info >> kInfoChunkShift) & 3) : g);
           }
         }
       };
@@ -835,6 +934,15 @@ void decode_attention_kernel(const Params p) {
   //    write) or this workgroup's piece of a segment cut at the share boundary
   //    (published as a partial).
   const int h = tid >> 4, d0 = (tid & 15) * DPT;
+  // Segment gv of sequence b: its rows, and the output row / query head of this
+  // thread's row h (multi-token runs: row 16 rc + h of the (sequence, KV head)).
+  auto seg_rows = [&](int b, int gv) {
+    return MULTI ? min(kPage, (s_ppre[b] & 31) * G - kPage * (gv % nrc)) : G;
+  };
+  auto out_row = [&](int b, int gv) { return MULTI ? (s_ppre[b] >> 5) + (kPage * (gv % nrc) + h) / G : b; };
+  auto out_head = [&](int gv) {
+    return MULTI ? s_qhead[(gv / nrc) * G + (kPage * (gv % nrc) + h) % G] : s_qhead[gv * G + h];
+  };
   int hand_seg[2] = {-1, -1};
   int nhand = 0;
   {
@@ -844,23 +952,24 @@ void decode_attention_kernel(const Params p) {
     for (int e = 0; e < DPT; ++e) o[e] = 0.f;
     // Close the group of segment `cur`: write it, or publish this workgroup's piece.
     auto flush = [&]() {
-      const int b = cur / Hkv, g = cur - b * Hkv;
+      const int b = cur / Hs, g = cur - b * Hs;   // g: the segment within the sequence
       const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
-      const int64_t seg_start = (int64_t)Hkv * pre_b + (int64_t)g * nb, seg_end = seg_start + nb;
+      const int64_t seg_start = (int64_t)Hs * pre_b + (int64_t)g * nb, seg_end = seg_start + nb;
       const bool whole = seg_start >= r0 && seg_end <= r1;
-      if (h < G) {
+      if (h < seg_rows(b, g)) {
         if (whole) {
-          store_out<D>(p, b, s_qhead[g * G + h], d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
+          store_out<D>(p, out_row(b, g), out_head(g), d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
         } else {
           const PartialRsrc rs = PartialRsrc::of<D>(p);
           const int gs = (seg_end > r1) ? 2 * u + 1 : 2 * u;
+          const int R = p.part_rows;
 #pragma unroll
           for (int c = 0; c < DPT; c += 4)
-            __builtin_amdgcn_raw_buffer_store_b128(*(const u32x4*)&o[c], rs.acc, ((gs * G + h) * D + d0 + c) * 4, 0,
+            __builtin_amdgcn_raw_buffer_store_b128(*(const u32x4*)&o[c], rs.acc, ((gs * R + h) * D + d0 + c) * 4, 0,
                                                    kDeviceScope);
           if ((tid & 15) == 0)
             __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(M), __float_as_uint(Ls)}, rs.ml,
-                                                  (gs * G + h) * 8, 0, kDeviceScope);
+                                                  (gs * R + h) * 8, 0, kDeviceScope);
         }
       }
       if (!whole && nhand < 2) hand_seg[nhand++] = cur;   // only the first and last group can be cut
@@ -888,7 +997,7 @@ void decode_attention_kernel(const Params p) {
 #pragma unroll
         for (int e = 0; e < DPT; ++e) o[e] = 0.f;
       }
-      if (sj >= 0 && h < G) lse_merge<DPT>(M, Ls, o, mj, lj, v);
+      if (sj >= 0 && h < seg_rows(sj / Hs, sj - (sj / Hs) * Hs)) lse_merge<DPT>(M, Ls, o, mj, lj, v);
     }
   }
 
@@ -899,9 +1008,9 @@ void decode_attention_kernel(const Params p) {
   __syncthreads();                 // ... and every other wave's
   if (tid < nhand) {
     const int sgi = hand_seg[tid];
-    const int b = sgi / Hkv, g = sgi - b * Hkv;
+    const int b = sgi / Hs, g = sgi - b * Hs;
     const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
-    const int64_t seg_start = (int64_t)Hkv * pre_b + (int64_t)g * nb;
+    const int64_t seg_start = (int64_t)Hs * pre_b + (int64_t)g * nb;
     const uint32_t npieces = (uint32_t)(owner_of(seg_start + nb - 1, Wn, T) - owner_of(seg_start, Wn, T) + 1);
     s_last[tid] = (atomicAdd(p.counters + sgi, 1u) + 1u == npieces);
   }
@@ -909,10 +1018,12 @@ void decode_attention_kernel(const Params p) {
   for (int i = 0; i < nhand; ++i) {
     if (!s_last[i]) continue;
     const int sgi = hand_seg[i];
-    const int b = sgi / Hkv, g = sgi - b * Hkv;
+    const int b = sgi / Hs, g = sgi - b * Hs;
     const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
-    const int64_t seg_start = (int64_t)Hkv * pre_b + (int64_t)g * nb;
-    if (h < G) merge_pieces<D>(p, b, g, h, d0, owner_of(seg_start, Wn, T), owner_of(seg_start + nb - 1, Wn, T));
+    const int64_t seg_start = (int64_t)Hs * pre_b + (int64_t)g * nb;
+    if (h < seg_rows(b, g))
+      merge_pieces<D>(p, out_row(b, g), out_head(g), h, d0, owner_of(seg_start, Wn, T),
+                      owner_of(seg_start + nb - 1, Wn, T));
     if (tid == 0) atomicExch(p.counters + sgi, 0u);
   }
 }
@@ -1202,11 +1313,11 @@ int launch_append_t(const Params& p, void* stream) {
   return (int)hipGetLastError();
 }
 
-template <class Pol>
+template <class Pol, bool MULTI = false>
 int launch(const Params& p, void* stream, void* ev_begin, void* ev_end) {
   hipStream_t st = (hipStream_t)stream;
   if (ev_begin && hipEventRecord((hipEvent_t)ev_begin, st) != hipSuccess) return -1;
-  hipLaunchKernelGGL(decode_attention_kernel<Pol>, dim3(p.nranges), dim3(kThreads), 0, st, p);
+  hipLaunchKernelGGL((decode_attention_kernel<Pol, MULTI>), dim3(p.nranges), dim3(kThreads), 0, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
   if (ev_end && hipEventRecord((hipEvent_t)ev_end, st) != hipSuccess) return -1;
@@ -1243,6 +1354,20 @@ int launch_prompt_then_decode(const Params& p, int ngroups, void* stream, void* 
 int launch_decode(KvKind kind, int head_dim, int group, const Params& p, void* stream, void* ev_begin,
                   void* ev_end) {
   RLDA_DISPATCH(launch, p, stream, ev_begin, ev_end)
+}
+
+int launch_decode_rows(KvKind kind, int head_dim, const Params& p, void* stream, void* ev_begin, void* ev_end) {
+  switch (kind) {
+    case KvKind::BF16:
+      return head_dim == 128 ? launch<Mfma<128, false>, true>(p, stream, ev_begin, ev_end)
+                             : launch<Mfma<64, false>, true>(p, stream, ev_begin, ev_end);
+    case KvKind::FP8:
+      return head_dim == 128 ? launch<Mfma<128, true>, true>(p, stream, ev_begin, ev_end)
+                             : launch<Mfma<64, true>, true>(p, stream, ev_begin, ev_end);
+    case KvKind::F32:
+      break;
+  }
+  return -1;
 }
 
 int launch_append(KvKind kind, int head_dim, const Params& p, void* stream) {

@@ -11,6 +11,9 @@ constexpr int kMaxQHeads = 256;
 constexpr int kMaxBatch = 8192;
 constexpr int kMaxRanges = 4096;   // upper bound on work ranges (= workgroups)
 constexpr int kMaxGroup = 16;      // query heads per KV head packed in one MFMA tile
+constexpr int kMaxRowChunks = 4;   // multi-token rows through the decode kernel: up to 4 x 16 per (sequence, KV head)
+constexpr int kMaxRowsQLen = 16;   // ... and at most 16 rows per sequence (a full page's token count, clamped
+                                   // to 31, less a row's causal shift of up to 15 still covers the page)
 
 // Bits of the device-side contract flag word.
 constexpr uint32_t kFlagBadPage = 1u;
@@ -26,8 +29,9 @@ struct Params {
   const int32_t* block_table;  // [batch][max_pages]
   const int32_t* seq_lens;     // [batch]
   void* out;                   // [batch][Hq][D]
-  float* part_acc;             // [2 * nranges][G][D]  unnormalised partial outputs
-  float* part_ml;              // [2 * nranges][G][2]  (running max in log2 units, sum)
+  float* part_acc;             // [2 * nranges][part_rows][D]  unnormalised partial outputs
+  float* part_ml;              // [2 * nranges][part_rows][2]  (running max in log2 units, sum)
+  int32_t part_rows;           // query rows per (sequence, KV head) segment: G, or n_max * G for multi-token rows
   uint32_t* counters;          // [max_batch * Hkv] finished pieces per split segment; zero between runs
   uint32_t* flags;             // contract-violation bits
   int64_t stride_page;         // bytes
@@ -58,6 +62,8 @@ struct Params {
   // Multi-token queries (rl_decode_attn_run_multi): q and out are [total_q][Hq][D].
   const int32_t* q_start;      // [batch + 1] query-row offsets
   int32_t total_q;
+  int32_t max_q_len;           // decode-kernel path: rows per sequence allowed (n_b <= max_q_len)
+  int32_t row_chunks;          // decode-kernel path: 16-row segments per (sequence, KV head), ceil(max_q_len * G / 16)
   int16_t q_head[kMaxQHeads];  // q_head[g * G + i] = i-th query head of KV head g
 };
 
@@ -75,6 +81,9 @@ int launch_grouped(KvKind kind, int head_dim, int group, const Params& p, int ng
 int launch_append(KvKind kind, int head_dim, const Params& p, void* stream);
 // Multi-token queries (rlda_multi.hip): one workgroup per (128-row query block, KV head).
 int launch_multi(KvKind kind, int head_dim, const Params& p, int grid, void* stream, void* ev_begin, void* ev_end);
+// Multi-token queries with at most 16 rows per (sequence, KV head) segment: the
+// decode kernel's page stream, each segment's rows masked causally (bf16 / fp8).
+int launch_decode_rows(KvKind kind, int head_dim, const Params& p, void* stream, void* ev_begin, void* ev_end);
 #ifndef RLDA_MQ_TILES
 #define RLDA_MQ_TILES 1            // 32-row MFMA tiles per wave in the multi-token kernel
 #endif

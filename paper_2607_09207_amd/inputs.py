@@ -372,9 +372,20 @@ def chunked_prefill_gqa_bf16(seed=1006, chunk=512):
     return with_query_rows(w, np.minimum(lens, chunk))
 
 
+def verify_gqa_bf16(seed=1007, rows=4):
+    """Verification of draft tokens on the long-tail GQA cache: the 64 sequences of
+    the GQA workload (28 query / 4 KV heads, d=128, bf16, lognormal median 2048,
+    sigma 1.0, clipped to [32, 16384]), each with its last `rows` tokens as query rows."""
+    rng = np.random.default_rng(seed)
+    lens = _lognormal_lengths(rng, 64, 2048, 1.0, 32, 16384)
+    w = _scattered("verify_gqa_bf16", seed, rng, lens, 28, 4, 128, "bf16", "bf16", 1024)
+    return with_query_rows(w, np.minimum(lens, rows))
+
+
 MULTI_WORKLOADS = {
     "prompt_prefill_grpo_bf16": prompt_prefill_grpo_bf16,
     "chunked_prefill_gqa_bf16": chunked_prefill_gqa_bf16,
+    "verify_gqa_bf16": verify_gqa_bf16,
 }
 
 

@@ -142,9 +142,10 @@ def test_destroy_null_and_strerror(lib):
     assert lib.rl_decode_attn_strerror(7) == b"unknown status"
 
 
-def test_workspace_grows_with_forced_ranges_and_heads(lib):
+def test_workspace_grows_with_forced_ranges_and_kv_heads(lib):
+    # partial slots per work range (16 rows each), counters per (sequence, KV head)
     sizes = []
-    for kw in [dict(num_work_ranges=16), dict(num_work_ranges=512), dict(num_work_ranges=512, num_q_heads=64, num_kv_heads=4)]:
+    for kw in [dict(num_work_ranges=16), dict(num_work_ranges=512), dict(num_work_ranges=512, num_q_heads=64, num_kv_heads=8)]:
         st, h = create(lib, cfg(**kw))
         n = ctypes.c_size_t()
         lib.rl_decode_attn_workspace_size(h, ctypes.byref(n))
@@ -216,8 +217,8 @@ def test_multi_rejects_bad_arguments_before_launch(lib):
     lib.rl_decode_attn_workspace_size(h, ctypes.byref(n))
     f = 0x10000
 
-    def multi(batch=4, total=100, q=f, ks=f, qs=f, out=f, ws=f * 16, wsb=None, e0=None, e1=None, handle=h):
-        return lib.rl_decode_attn_run_multi(handle, batch, 10, total, q, f, f, ks, f, f, f, qs, out, ws,
+    def multi(batch=4, total=100, q=f, ks=f, qs=f, out=f, ws=f * 16, wsb=None, e0=None, e1=None, handle=h, mq=0):
+        return lib.rl_decode_attn_run_multi(handle, batch, 10, total, mq, q, f, f, ks, f, f, f, qs, out, ws,
                                             n.value if wsb is None else wsb, None, e0, e1)
 
     assert multi(q=None) == -1
@@ -231,6 +232,10 @@ def test_multi_rejects_bad_arguments_before_launch(lib):
     assert multi(ws=None) == -4
     assert multi(wsb=n.value - 1) == -4
     assert multi(batch=4097) == -2        # beyond the multi-token kernel's batch limit
+    assert multi(mq=-1) == -1
+    # max_q_len beyond what the decode kernel's rows path takes (17 rows; 10 * G = 70
+    # rows > 64): the multi-token kernel, with its batch limit
+    assert multi(batch=4097, mq=17) == -2 and multi(batch=4097, mq=10) == -2
     assert multi(total=(1 << 31) // (28 * 128 * 2) + 1) == -2   # q beyond 2^31 bytes
     assert multi(batch=0) == 0 and multi(total=0) == 0
     lib.rl_decode_attn_destroy(h)

@@ -26,15 +26,15 @@ def torch_cuda():
     return torch
 
 
-def run_multi(torch, w, out_dtype="f32", handle=None, tag="", out=None):
+def run_multi(torch, w, out_dtype="f32", handle=None, tag="", out=None, max_q_len=0):
     log(f"{tag} multi B={w.batch} Hq={w.num_q_heads} Hkv={w.num_kv_heads} d={w.head_dim} kv={w.kv_dtype} "
         f"layout={w.layout} rows={int(w.q_start[-1])} q_lens={np.diff(w.q_start)[:8].tolist()} "
-        f"lens={w.seq_lens[:8].tolist()} out={out_dtype}")
+        f"lens={w.seq_lens[:8].tolist()} out={out_dtype} max_q_len={max_q_len}")
     t = I.to_torch(w, "cuda")
     qs = torch.from_numpy(np.ascontiguousarray(w.q_start, np.int32)).cuda()
     h = handle or handle_for(w, out_dtype)
     res = h.multi(t["q"], t["k_cache"], t["v_cache"], t["block_table"], t["seq_lens"], qs, k_scale=t["k_scale"],
-                  v_scale=t["v_scale"], out=out)
+                  v_scale=t["v_scale"], out=out, max_q_len=max_q_len)
     torch.cuda.synchronize()
     flags = h.read_flags(device=res.device)
     return res.float().cpu().numpy().astype(np.float64), flags
