@@ -352,10 +352,14 @@ rlda_status rl_decode_attn_run_multi(rl_decode_attn_t h, int32_t batch, int32_t 
   if ((!event_begin) != (!event_end)) return RLDA_ERR_INVALID_ARG;
   if (h->kind == rlda::KvKind::F32) return RLDA_ERR_UNSUPPORTED;
   // Few rows per sequence: the decode kernel's page stream, which splits long
-  // sequences across workgroups, each (sequence, KV head) as up to 4 segments of
-  // 16 rows.  Otherwise the 128-row MFMA kernel.
-  const int64_t row_chunks = ((int64_t)max_q_len * h->group + rlda::kMaxGroup - 1) / rlda::kMaxGroup;
-  const bool rows_path = max_q_len >= 1 && max_q_len <= rlda::kMaxRowsQLen && row_chunks <= rlda::kMaxRowChunks &&
+  // sequences across workgroups.  The rows of a (sequence, KV head), at most 64,
+  // are held by a wave as one or two 16-row tiles against each page; more than 32
+  // take two segments.  Otherwise the 128-row MFMA kernel.
+  const int64_t rows = (int64_t)max_q_len * h->group;
+  int tiles = rows > rlda::kMaxGroup ? rlda::kMaxRowTiles : 1;
+  int64_t row_chunks = (rows + rlda::kMaxGroup * tiles - 1) / (rlda::kMaxGroup * tiles);
+  const bool rows_path = max_q_len >= 1 && max_q_len <= rlda::kMaxRowsQLen &&
+                         rows <= (int64_t)rlda::kMaxGroup * rlda::kMaxRowChunks &&
                          (int64_t)batch * c.max_pages_per_seq * c.num_kv_heads * row_chunks <= INT32_MAX;
   if (!rows_path && batch > rlda::kMultiMaxBatch) return RLDA_ERR_UNSUPPORTED;
   // The kernels address q with 32-bit byte offsets.
@@ -405,10 +409,17 @@ rlda_status rl_decode_attn_run_multi(rl_decode_attn_t h, int32_t batch, int32_t 
     if (hipGetDevice(&dev) != hipSuccess) return RLDA_ERR_HIP;
     int ranges = c.num_work_ranges > 0 ? c.num_work_ranges : cu_count(dev);
     if (ranges <= 0) return RLDA_ERR_HIP;
-    // Partial slots hold one segment's rows (at most 16) each.
+    // Partial slots hold one segment's rows each; the workspace has room for
+    // 2 * ws_ranges * 16 rows.  A workspace sized for fewer ranges than two-tile
+    // slots need falls back to one tile per segment.
+    if (tiles == 2 && (int64_t)h->ws_ranges * rlda::kMaxGroup / std::min<int64_t>(rows, 32) < 1) {
+      tiles = 1;
+      row_chunks = (rows + rlda::kMaxGroup - 1) / rlda::kMaxGroup;
+    }
     p.row_chunks = (int)row_chunks;
-    p.part_rows = std::min<int>(max_q_len * h->group, rlda::kMaxGroup);
-    if (ranges > h->ws_ranges) ranges = h->ws_ranges;
+    p.part_rows = (int)std::min<int64_t>(rows, (int64_t)rlda::kMaxGroup * tiles);
+    const int64_t cap_ranges = (int64_t)h->ws_ranges * rlda::kMaxGroup / p.part_rows;
+    if (ranges > cap_ranges) ranges = (int)cap_ranges;
     if (ranges > rlda::kMaxRanges) ranges = rlda::kMaxRanges;
     const int64_t max_units = (int64_t)batch * c.num_kv_heads * row_chunks * c.max_pages_per_seq;
     if (ranges > max_units) ranges = (int)max_units;
@@ -417,7 +428,7 @@ rlda_status rl_decode_attn_run_multi(rl_decode_attn_t h, int32_t batch, int32_t 
     p.counters = (uint32_t*)(ws + wl.counters);
     p.part_ml = (float*)(ws + wl.part_ml);
     p.part_acc = (float*)(ws + wl.part_acc);
-    if (rlda::launch_decode_rows(h->kind, c.head_dim, p, stream, event_begin, event_end) != hipSuccess)
+    if (rlda::launch_decode_rows(h->kind, c.head_dim, tiles, p, stream, event_begin, event_end) != hipSuccess)
       return RLDA_ERR_HIP;
     return RLDA_OK;
   }

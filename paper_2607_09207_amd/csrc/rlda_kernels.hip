@@ -678,9 +678,10 @@ __device__ __forceinline__ StreamChunk fetch_chunk(const Params& p, const int32_
 // rows per (sequence, KV head)): (b, g) has n_b * G rows, row r is query head
 // (r % G) of query row q_start[b] + r / G and sees keys below L - n_b + r / G + 1;
 // its rows are streamed as row_chunks segments of 16 rows each.
-template <class Pol, bool MULTI = false>
+template <class Pol, bool MULTI = false, int NT = 1>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(1, 1)))
 void decode_attention_kernel(const Params p) {
+  static_assert(NT == 1 || (MULTI && NT == 2), "two row tiles only for multi-token rows");
   constexpr int D = Pol::kD;
   constexpr int DPT = D / 16;   // output elements per thread in the workgroup merge
   __shared__ int32_t s_pre[kMaxBatch + 1];
@@ -708,8 +709,10 @@ void decode_attention_kernel(const Params p) {
   }();
   const int batch = p.batch, Hkv = p.num_kv_heads, G = p.group;
   const int cap = p.max_pages * kPage;
-  // Multi-token runs: nrc 16-row segments per (sequence, KV head), Hs per sequence.
+  // Multi-token runs: nrc segments of 16 NT rows per (sequence, KV head), Hs per
+  // sequence; a wave holds NT 16-row tiles against each page of a segment.
   const int nrc = MULTI ? p.row_chunks : 1, Hs = Hkv * nrc;
+  constexpr int kSegRows = 16 * NT;
 
   // 1. Page counts per sequence and their prefix sums (identical in every workgroup).
   {
@@ -810,11 +813,18 @@ void decode_attention_kernel(const Params p) {
   //    written directly.
   const int64_t r0 = (int64_t)u * T / Wn, r1 = (int64_t)(u + 1) * T / Wn;
   const int w0 = (int)(r0 + (r1 - r0) * wave / kWaves), w1 = (int)(r0 + (r1 - r0) * (wave + 1) / kWaves);
+  // Two-tile segments: tile 1's running state, and tile 1 of the wave's first
+  // piece (slot 2w), both kept for the second pass of the workgroup merge.
+  Pol st2, held;
+  // Q operands of the NT tiles, loaded with a segment's first page.
+  struct QN {
+    typename Pol::QOp t[NT];
+  };
   if (w0 < w1) {
     constexpr int kDepth = Pol::kDepth;
     Pol st;
     st.setup(p, lane, p.stride_slot);
-    typename Pol::QOp qring[kDepth];
+    QN qring[kDepth];
     typename Pol::PInit pring[kDepth];
     bool began = false;   // the segment being accumulated began inside this quarter
     StreamChunk nxt = fetch_chunk<MULTI>(p, s_pre, s_tail, s_ppre, w0, w0, w1, lane, Hs, nrc);
@@ -826,8 +836,8 @@ void decode_attention_kernel(const Params p) {
       int sinfo[kDepth];
       float skm[kDepth], svm[kDepth];
       // Issue the loads of position base + k into pipeline slot `sl`.
-      auto issue = [&](typename Pol::Frag& f, int& info_out, float& km_out, float& vm_out,
-                       typename Pol::QOp& q_out, typename Pol::PInit& pi_out, int k) {
+      auto issue = [&](typename Pol::Frag& f, int& info_out, float& km_out, float& vm_out, QN& q_out,
+                       typename Pol::PInit& pi_out, int k) {
         int pk = -1, info = 0;
         float ks = 1.f, vs = 1.f;
         if (k < cn) {
@@ -853,11 +863,12 @@ void decode_attention_kernel(const Params p) {
         const uint32_t nrec = ptok > 0 ? (uint32_t)((ptok - 1) * p.stride_slot + D * Pol::kEB) : 0u;
         st.issue(f, make_rsrc_uni((const char*)p.k + po, nrec), make_rsrc_uni((const char*)p.v + po, nrec));
         if constexpr (MULTI) {
-          const int qs = s_ppre[b];
-          Pol::load_q_multi(q_out, p, qs >> 5, qs & 31, g, kPage * ((info >> kInfoChunkShift) & 3), lane,
-                            (info & (kInfoFirst | kInfoStart)) != 0);
+          const int qs = s_ppre[b], rb = kSegRows * ((info >> kInfoChunkShift) & 3);
+          const bool ld = (info & (kInfoFirst | kInfoStart)) != 0;
+          Pol::load_q_multi(q_out.t[0], p, qs >> 5, qs & 31, g, rb, lane, ld);
+          if constexpr (NT == 2) Pol::load_q_multi(q_out.t[NT - 1], p, qs >> 5, qs & 31, g, rb + 16, lane, ld);
         } else if constexpr (Pol::kQRing) {
-          Pol::load_q(q_out, p, b, g, lane, (info & (kInfoFirst | kInfoStart)) != 0);
+          Pol::load_q(q_out.t[0], p, b, g, lane, (info & (kInfoFirst | kInfoStart)) != 0);
           Pol::load_prompt(pi_out, p, b, g, lane, (info & kInfoFirst) && (info & kInfoPrompt));
         }
         info_out = info;   // the scales are used as loaded, in compute
@@ -865,7 +876,7 @@ void decode_attention_kernel(const Params p) {
         vm_out = vs;
       };
       // Consume pipeline slot `sl` (position base + k).
-      auto compute = [&](const typename Pol::Frag& f, int info, float km, float vm, const typename Pol::QOp& q,
+      auto compute = [&](const typename Pol::Frag& f, int info, float km, float vm, const QN& q,
                          const typename Pol::PInit& pi, int k) {
         if (k >= cn) return;
         const int g = (info >> kInfoHeadShift) & 255, b = (info >> kInfoSeqShift) & 8191;
@@ -873,31 +884,42 @@ void decode_attention_kernel(const Params p) {
           bool seeded = false;
           if constexpr (Pol::kQRing && !MULTI) {
             if ((info & kInfoFirst) && (info & kInfoPrompt)) {
-              st.begin_prompt(q, pi, G, lane);
+              st.begin_prompt(q.t[0], pi, G, lane);
               seeded = true;
             }
           }
-          if (!seeded) st.begin(q, p, b, g, lane);
+          if (!seeded) st.begin(q.t[0], p, b, g, lane);
           if constexpr (MULTI) {
-            const int nq = s_ppre[b] & 31, r = kPage * ((info >> kInfoChunkShift) & 3) + (lane & 15);
+            const int nq = s_ppre[b] & 31, r = kSegRows * ((info >> kInfoChunkShift) & 3) + (lane & 15);
             st.shift = (r < nq * G) ? nq - 1 - r / G : 0;
+            if constexpr (NT == 2) {
+              st2.begin(q.t[NT - 1], p, b, g, lane);
+              st2.shift = (r + 16 < nq * G) ? nq - 1 - (r + 16) / G : 0;
+            }
           }
           began = (info & kInfoFirst) != 0;
         }
-        if constexpr (MULTI)
+        if constexpr (MULTI) {
           st.template compute<true>(f, lane, info & kInfoTok, p.scale_log2 * km, vm);
-        else
+          if constexpr (NT == 2) st2.template compute<true>(f, lane, info & kInfoTok, p.scale_log2 * km, vm);
+        } else
           st.compute(f, lane, info & kInfoTok, p.scale_log2 * km, vm);
         if (info & (kInfoLast | kInfoEnd)) {
           const bool ended = (info & kInfoLast) != 0;
           if (began && ended) {
-            if constexpr (MULTI)
-              st.write_out_multi(p, s_ppre[b] >> 5, s_ppre[b] & 31, g, kPage * ((info >> kInfoChunkShift) & 3), lane);
-            else
+            if constexpr (MULTI) {
+              const int rb = kSegRows * ((info >> kInfoChunkShift) & 3);
+              st.write_out_multi(p, s_ppre[b] >> 5, s_ppre[b] & 31, g, rb, lane);
+              if constexpr (NT == 2) st2.write_out_multi(p, s_ppre[b] >> 5, s_ppre[b] & 31, g, rb + 16, lane);
+            } else {
               st.write_out(p, b, g, lane);
+            }
           } else {
             const int slot = 2 * wave + (ended ? 0 : 1);
             st.to_lds(s_acc[slot], s_ml[slot], lane);
+            if constexpr (NT == 2) {
+              if (ended) held = st2;   // slot 2w+1 is the quarter's last piece: st2 keeps it
+            }
             if (lane == 0) s_seg[slot] = b * Hs + (MULTI ? g * nrc + ((info >> kInfoChunkShift) & 3) : g);
           }
         }
@@ -934,18 +956,30 @@ void decode_attention_kernel(const Params p) {
   //    write) or this workgroup's piece of a segment cut at the share boundary
   //    (published as a partial).
   const int h = tid >> 4, d0 = (tid & 15) * DPT;
-  // Segment gv of sequence b: its rows, and the output row / query head of this
-  // thread's row h (multi-token runs: row 16 rc + h of the (sequence, KV head)).
-  auto seg_rows = [&](int b, int gv) {
-    return MULTI ? min(kPage, (s_ppre[b] & 31) * G - kPage * (gv % nrc)) : G;
+  // Tile t of segment gv of sequence b: its rows, and the output row / query head
+  // of this thread's row h (multi-token runs: row 16 NT rc + 16 t + h of the
+  // (sequence, KV head)).
+  auto seg_row = [&](int gv, int t) { return kSegRows * (gv % nrc) + 16 * t + h; };
+  auto seg_rows = [&](int b, int gv, int t) {
+    return MULTI ? min(kPage, (s_ppre[b] & 31) * G - kSegRows * (gv % nrc) - 16 * t) : G;
   };
-  auto out_row = [&](int b, int gv) { return MULTI ? (s_ppre[b] >> 5) + (kPage * (gv % nrc) + h) / G : b; };
-  auto out_head = [&](int gv) {
-    return MULTI ? s_qhead[(gv / nrc) * G + (kPage * (gv % nrc) + h) % G] : s_qhead[gv * G + h];
+  auto out_row = [&](int b, int gv, int t) { return MULTI ? (s_ppre[b] >> 5) + seg_row(gv, t) / G : b; };
+  auto out_head = [&](int gv, int t) {
+    return MULTI ? s_qhead[(gv / nrc) * G + seg_row(gv, t) % G] : s_qhead[gv * G + h];
   };
   int hand_seg[2] = {-1, -1};
   int nhand = 0;
-  {
+  // One pass per row tile; the second pass merges the tile-1 states of the same slots.
+#pragma unroll 1
+  for (int t = 0; t < NT; ++t) {
+    if constexpr (NT == 2) {
+      if (t > 0) {
+        __syncthreads();   // the first pass has read the slots
+        if (s_seg[2 * wave] != -1) held.to_lds(s_acc[2 * wave], s_ml[2 * wave], lane);
+        if (s_seg[2 * wave + 1] != -1) st2.to_lds(s_acc[2 * wave + 1], s_ml[2 * wave + 1], lane);
+        __syncthreads();
+      }
+    }
     int cur = -1;   // segment of the group being merged
     float M = neg_inf(), Ls = 0.f, o[DPT];
 #pragma unroll
@@ -956,23 +990,24 @@ void decode_attention_kernel(const Params p) {
       const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
       const int64_t seg_start = (int64_t)Hs * pre_b + (int64_t)g * nb, seg_end = seg_start + nb;
       const bool whole = seg_start >= r0 && seg_end <= r1;
-      if (h < seg_rows(b, g)) {
+      if (h < seg_rows(b, g, t)) {
         if (whole) {
-          store_out<D>(p, out_row(b, g), out_head(g), d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
+          store_out<D>(p, out_row(b, g, t), out_head(g, t), d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
         } else {
           const PartialRsrc rs = PartialRsrc::of<D>(p);
           const int gs = (seg_end > r1) ? 2 * u + 1 : 2 * u;
-          const int R = p.part_rows;
+          const int R = p.part_rows, hr = 16 * t + h;   // the row within the slot
 #pragma unroll
           for (int c = 0; c < DPT; c += 4)
-            __builtin_amdgcn_raw_buffer_store_b128(*(const u32x4*)&o[c], rs.acc, ((gs * R + h) * D + d0 + c) * 4, 0,
+            __builtin_amdgcn_raw_buffer_store_b128(*(const u32x4*)&o[c], rs.acc, ((gs * R + hr) * D + d0 + c) * 4, 0,
                                                    kDeviceScope);
           if ((tid & 15) == 0)
             __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(M), __float_as_uint(Ls)}, rs.ml,
-                                                  (gs * R + h) * 8, 0, kDeviceScope);
+                                                  (gs * R + hr) * 8, 0, kDeviceScope);
         }
       }
-      if (!whole && nhand < 2) hand_seg[nhand++] = cur;   // only the first and last group can be cut
+      // Only the first and last group can be cut; the second pass sees the same groups.
+      if (t == 0 && !whole && nhand < 2) hand_seg[nhand++] = cur;
     };
     // Slots in position order; the used slots of one segment are consecutive.  Each
     // step issues its LDS reads (tag, max/sum, partial output) together.
@@ -997,7 +1032,7 @@ void decode_attention_kernel(const Params p) {
 #pragma unroll
         for (int e = 0; e < DPT; ++e) o[e] = 0.f;
       }
-      if (sj >= 0 && h < seg_rows(sj / Hs, sj - (sj / Hs) * Hs)) lse_merge<DPT>(M, Ls, o, mj, lj, v);
+      if (sj >= 0 && h < seg_rows(sj / Hs, sj - (sj / Hs) * Hs, t)) lse_merge<DPT>(M, Ls, o, mj, lj, v);
     }
   }
 
@@ -1021,9 +1056,11 @@ void decode_attention_kernel(const Params p) {
     const int b = sgi / Hs, g = sgi - b * Hs;
     const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
     const int64_t seg_start = (int64_t)Hs * pre_b + (int64_t)g * nb;
-    if (h < seg_rows(b, g))
-      merge_pieces<D>(p, out_row(b, g), out_head(g), h, d0, owner_of(seg_start, Wn, T),
-                      owner_of(seg_start + nb - 1, Wn, T));
+#pragma unroll 1
+    for (int t = 0; t < NT; ++t)
+      if (h < seg_rows(b, g, t))
+        merge_pieces<D>(p, out_row(b, g, t), out_head(g, t), 16 * t + h, d0, owner_of(seg_start, Wn, T),
+                        owner_of(seg_start + nb - 1, Wn, T));
     if (tid == 0) atomicExch(p.counters + sgi, 0u);
   }
 }
@@ -1313,11 +1350,11 @@ int launch_append_t(const Params& p, void* stream) {
   return (int)hipGetLastError();
 }
 
-template <class Pol, bool MULTI = false>
+template <class Pol, bool MULTI = false, int NT = 1>
 int launch(const Params& p, void* stream, void* ev_begin, void* ev_end) {
   hipStream_t st = (hipStream_t)stream;
   if (ev_begin && hipEventRecord((hipEvent_t)ev_begin, st) != hipSuccess) return -1;
-  hipLaunchKernelGGL((decode_attention_kernel<Pol, MULTI>), dim3(p.nranges), dim3(kThreads), 0, st, p);
+  hipLaunchKernelGGL((decode_attention_kernel<Pol, MULTI, NT>), dim3(p.nranges), dim3(kThreads), 0, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
   if (ev_end && hipEventRecord((hipEvent_t)ev_end, st) != hipSuccess) return -1;
@@ -1356,14 +1393,20 @@ int launch_decode(KvKind kind, int head_dim, int group, const Params& p, void* s
   RLDA_DISPATCH(launch, p, stream, ev_begin, ev_end)
 }
 
-int launch_decode_rows(KvKind kind, int head_dim, const Params& p, void* stream, void* ev_begin, void* ev_end) {
+template <class Pol>
+int launch_rows(int tiles, const Params& p, void* stream, void* ev_begin, void* ev_end) {
+  return tiles == 2 ? launch<Pol, true, 2>(p, stream, ev_begin, ev_end) : launch<Pol, true, 1>(p, stream, ev_begin, ev_end);
+}
+
+int launch_decode_rows(KvKind kind, int head_dim, int tiles, const Params& p, void* stream, void* ev_begin,
+                       void* ev_end) {
   switch (kind) {
     case KvKind::BF16:
-      return head_dim == 128 ? launch<Mfma<128, false>, true>(p, stream, ev_begin, ev_end)
-                             : launch<Mfma<64, false>, true>(p, stream, ev_begin, ev_end);
+      return head_dim == 128 ? launch_rows<Mfma<128, false>>(tiles, p, stream, ev_begin, ev_end)
+                             : launch_rows<Mfma<64, false>>(tiles, p, stream, ev_begin, ev_end);
     case KvKind::FP8:
-      return head_dim == 128 ? launch<Mfma<128, true>, true>(p, stream, ev_begin, ev_end)
-                             : launch<Mfma<64, true>, true>(p, stream, ev_begin, ev_end);
+      return head_dim == 128 ? launch_rows<Mfma<128, true>>(tiles, p, stream, ev_begin, ev_end)
+                             : launch_rows<Mfma<64, true>>(tiles, p, stream, ev_begin, ev_end);
     case KvKind::F32:
       break;
   }

@@ -12,6 +12,10 @@ constexpr int kMaxBatch = 8192;
 constexpr int kMaxRanges = 4096;   // upper bound on work ranges (= workgroups)
 constexpr int kMaxGroup = 16;      // query heads per KV head packed in one MFMA tile
 constexpr int kMaxRowChunks = 4;   // multi-token rows through the decode kernel: up to 4 x 16 per (sequence, KV head)
+#ifndef RLDA_MAX_ROW_TILES
+#define RLDA_MAX_ROW_TILES 2       // 16-row tiles a wave holds against each page on that path (1 or 2)
+#endif
+constexpr int kMaxRowTiles = RLDA_MAX_ROW_TILES;
 constexpr int kMaxRowsQLen = 16;   // ... and at most 16 rows per sequence (a full page's token count, clamped
                                    // to 31, less a row's causal shift of up to 15 still covers the page)
 
@@ -63,7 +67,7 @@ struct Params {
   const int32_t* q_start;      // [batch + 1] query-row offsets
   int32_t total_q;
   int32_t max_q_len;           // decode-kernel path: rows per sequence allowed (n_b <= max_q_len)
-  int32_t row_chunks;          // decode-kernel path: 16-row segments per (sequence, KV head), ceil(max_q_len * G / 16)
+  int32_t row_chunks;          // decode-kernel path: segments per (sequence, KV head), ceil(max_q_len * G / (16 * tiles))
   int16_t q_head[kMaxQHeads];  // q_head[g * G + i] = i-th query head of KV head g
 };
 
@@ -81,9 +85,10 @@ int launch_grouped(KvKind kind, int head_dim, int group, const Params& p, int ng
 int launch_append(KvKind kind, int head_dim, const Params& p, void* stream);
 // Multi-token queries (rlda_multi.hip): one workgroup per (128-row query block, KV head).
 int launch_multi(KvKind kind, int head_dim, const Params& p, int grid, void* stream, void* ev_begin, void* ev_end);
-// Multi-token queries with at most 16 rows per (sequence, KV head) segment: the
-// decode kernel's page stream, each segment's rows masked causally (bf16 / fp8).
-int launch_decode_rows(KvKind kind, int head_dim, const Params& p, void* stream, void* ev_begin, void* ev_end);
+// Multi-token queries with at most 16 * tiles rows per (sequence, KV head) segment
+// (tiles 1 or 2): the decode kernel's page stream, each row masked causally (bf16 / fp8).
+int launch_decode_rows(KvKind kind, int head_dim, int tiles, const Params& p, void* stream, void* ev_begin,
+                       void* ev_end);
 #ifndef RLDA_MQ_TILES
 #define RLDA_MQ_TILES 1            // 32-row MFMA tiles per wave in the multi-token kernel
 #endif

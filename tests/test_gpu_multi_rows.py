@@ -134,3 +134,16 @@ def test_rows_path_maximum_batch(torch_cuda):
     got, flags = run_multi(torch_cuda, w, tag="rows max batch", max_q_len=2)
     assert flags == 0
     assert_close(got, oracle.run_multi(w), "bf16", "rows path max batch 8192")
+
+
+@pytest.mark.parametrize("ranges", [2, 5])
+def test_rows_path_two_tiles_many_short_sequences(torch_cuda, ranges):
+    # 28 rows per (sequence, KV head): two tiles per wave; many whole segments inside
+    # each wave's quarter and cut ones at its ends, on two merge passes
+    rng = np.random.default_rng(48)
+    lens = rng.integers(4, 120, size=40).tolist() + [900, 37]
+    w = I.make_multi(lens, [4] * len(lens), 28, 4, 128, q_dtype="bf16", kv_dtype="bf16", seed=49)
+    h = handle_for(w, ranges=ranges)
+    got, flags = run_multi(torch_cuda, w, handle=h, tag=f"rows two tiles ranges={ranges}", max_q_len=4)
+    assert flags == 0
+    assert_close(got, oracle.run_multi(w), "bf16", f"rows path two tiles ranges={ranges}")
