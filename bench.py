@@ -275,8 +275,9 @@ def main():
                     help="multi mode: bound on query rows per sequence passed to run_multi (0: none)")
     ap.add_argument("--prompt-tokens", type=int, default=0,
                     help="GRPO workload only: prompt length shared by each group (default 512)")
-    ap.add_argument("--grouped", choices=["on", "off"], default="off",
-                    help="on: the shared-prompt entry point (rl_decode_attn_run_grouped) for GRPO workloads")
+    ap.add_argument("--grouped", choices=["auto", "on", "off"], default="auto",
+                    help="on: the shared-prompt entry point (rl_decode_attn_run_grouped) for GRPO workloads; "
+                         "auto: on exactly when the workload's groups share prompt pages")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (this path needs no "
@@ -322,7 +323,8 @@ def main():
         s["v_cache"] = sets[0]["v_cache"].clone()
         sets.append(s)
     out = torch.empty((w.batch, w.num_q_heads, w.head_dim), dtype=torch.float32, device=dev)
-    grouped = args.grouped == "on"
+    shares_prompt = w.shared_prefix_tokens > 0 and w.group_size > 1
+    grouped = args.grouped == "on" or (args.grouped == "auto" and shares_prompt)
     gkw = {}
     if grouped:
         if not (w.shared_prefix_tokens > 0 and w.group_size > 1):
@@ -402,7 +404,7 @@ def main():
             "hbm_frac": round(value / PEAK_HBM_GBS, 4),
             "sequences_per_s": round(w.batch / (ms_per_step * 1e-3), 1),
             "kv_sets_rotated": len(sets),
-            "shared_prompt_pass": grouped,
+            "entry_point": "rl_decode_attn_run_grouped" if grouped else "rl_decode_attn_run",
         },
         "roofline": {
             "bound": "hbm",

@@ -142,10 +142,18 @@ rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t handle, int32_t batch, 
  * form group i; the first prefix_pages[i] entries of their block-table rows name
  * the same pool pages (the prompt), each holding page_size valid tokens.  The
  * result is that of rl_decode_attn_run on the same arguments (up to rounding
- * order), but each prompt page is read once per KV head for the whole group: a
- * prompt pass multiplies it against the query rows of up to 64/G members at once
- * (up to four 16-row MFMA tiles), and the attention over the remaining pages of
- * each sequence starts from the prompt pass's (max, sum, output) state.
+ * order), but prompt pages are read fewer times.  Two ways, chosen on the host:
+ *   - packed (at least two members fit the 16 rows of one MFMA tile: 2G <= 16,
+ *     group_size >= 2, batch <= 4096, max_pages_per_seq <= 32767): one kernel.
+ *     Up to min(7, 16/G) consecutive members of a group form a pack whose rows
+ *     share one tile; the pack's segment streams the prompt pages once with every
+ *     member's rows, then each member's own pages with only its rows unmasked.
+ *     Each prompt page is read once per pack and KV head.
+ *   - otherwise: a prompt pass multiplies each prompt page against the query rows
+ *     of up to 64/G members at once (up to four 16-row MFMA tiles), and the
+ *     attention over the remaining pages of each sequence starts from the prompt
+ *     pass's (max, sum, output) state.  Each prompt page is read once per group
+ *     and KV head.
  *   group_size    >= 1, host value
  *   prefix_pages  [ceil(batch / group_size)] int32, device memory
  * The prompt pages are read from the block-table row of the group's first
@@ -156,10 +164,10 @@ rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t handle, int32_t batch, 
  * raises flag bit 2; prefix_pages[i] = 0 shares nothing for group i.
  * Supported for bf16 and fp8 caches (RLDA_ERR_UNSUPPORTED for f32).
  * workspace: >= rl_decode_attn_grouped_workspace_size bytes, same rules as for
- * rl_decode_attn_run (the same workspace serves both calls).  Two kernels are
- * queued on `stream`: the prompt pass, then the attention over the rest.
- * event_begin / event_end (hipEvent_t): both NULL, or both given to be recorded
- * before the first and after the second kernel.
+ * rl_decode_attn_run (the same workspace serves both calls).  One kernel (packed)
+ * or two (the prompt pass, then the attention over the rest) are queued on
+ * `stream`.  event_begin / event_end (hipEvent_t): both NULL, or both given to be
+ * recorded before the first and after the last kernel.
  */
 rlda_status rl_decode_attn_run_grouped(rl_decode_attn_t handle, int32_t batch, int32_t num_pages, int32_t group_size,
                                        const int32_t* prefix_pages, const void* q, const void* k_cache,

@@ -240,6 +240,26 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32
     return RLDA_OK;
   }
   p.prefix_pages = prefix_pages;
+  p.group_size = group_size;
+  // Packed: up to 16 * tiles / G members of a group share the rows of the MFMA
+  // tiles, so one segment streams the prompt pages once for all of them and then
+  // each member's own pages.  One launch, no prompt pass.
+  const int tiles = rlda::kPackTiles;
+  const int pack = std::min(std::min(rlda::kPackMaxMembers, rlda::kMaxGroup * tiles / h->group), group_size);
+  if (pack >= 2 && batch <= rlda::kPackMaxBatch && c.max_pages_per_seq <= rlda::kPackMaxPages) {
+    const int ngroups = (batch + group_size - 1) / group_size, per_group = (group_size + pack - 1) / pack;
+    const int last = batch - (ngroups - 1) * group_size;
+    p.pack = pack;
+    p.pack_units = (ngroups - 1) * per_group + (last + pack - 1) / pack;
+    p.total_q = batch;
+    p.row_chunks = 1;
+    p.part_rows = std::min(pack * h->group, rlda::kMaxGroup * tiles);
+    const int64_t cap_ranges = (int64_t)h->ws_ranges * rlda::kMaxGroup / p.part_rows;
+    if (p.nranges > cap_ranges) p.nranges = (int)std::max<int64_t>(cap_ranges, 1);
+    if (rlda::launch_decode_packed(h->kind, c.head_dim, tiles, p, stream, ev_begin, ev_end) != hipSuccess)
+      return RLDA_ERR_HIP;
+    return RLDA_OK;
+  }
   p.gprefix = (int32_t*)(ws + wl.gprefix);
   p.pfx_ml = (float*)(ws + wl.pfx_ml);
   p.pfx_acc = (float*)(ws + wl.pfx_acc);

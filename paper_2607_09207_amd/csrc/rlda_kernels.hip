@@ -630,6 +630,8 @@ constexpr int kInfoHeadShift = 9;       // KV head g: 8 bits
 constexpr int kInfoSeqShift = 17;       // sequence b: 13 bits (b < 8192)
 constexpr int kInfoPrompt = 1 << 30;    // grouped run: the sequence's prompt pass state seeds its first page
 constexpr int kInfoChunkShift = 30;     // multi-token run: the segment's 16-row chunk (2 bits)
+constexpr int kInfoActShift = 29;       // packed grouped run: the pack member whose rows the page serves (3 bits;
+constexpr int kActAll = 7;              // kActAll: a prompt page, every member's rows); the pack index has 12 bits
 
 // The page id is returned as read; it is checked where it is used, so that
 // nothing waits for these loads until the chunk is consumed.
@@ -645,15 +647,19 @@ struct StreamChunk {
 // need, and split a (sequence, KV head) with more than 16 rows into nrc segments
 // of 16 rows that each stream the pages: segment gv = g * nrc + rc of a sequence,
 // Hs = Hkv * nrc segments per sequence.
-template <bool MULTI>
+// Packed grouped runs: a unit is a pack of consecutive members of one GRPO group;
+// its segment streams the group's prompt pages once (every member's rows take
+// part), then each member's own pages in member order (only that member's rows).
+template <bool MULTI, bool PACK>
 __device__ __forceinline__ StreamChunk fetch_chunk(const Params& p, const int32_t* s_pre, const uint8_t* s_tail,
-                                                   const int32_t* s_ppre, int base, int w0, int w1, int lane, int Hs,
-                                                   int nrc) {
+                                                   const int32_t* s_ppre, const uint16_t* s_nfull,
+                                                   const int16_t* s_gpp, int nunits, int base, int w0, int w1,
+                                                   int lane, int Hs, int nrc) {
   StreamChunk c = {-1, 0};
   const int pos = base + lane;
   if (pos < w1) {
     const int y = (int)((uint32_t)pos / (uint32_t)Hs);
-    int lo = 0, hi = p.batch;   // s_pre[lo] <= y < s_pre[hi]
+    int lo = 0, hi = nunits;   // s_pre[lo] <= y < s_pre[hi]
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
       if (s_pre[mid] <= y) lo = mid; else hi = mid;
@@ -662,12 +668,38 @@ __device__ __forceinline__ StreamChunk fetch_chunk(const Params& p, const int32_
     const int off = pos - Hs * pre;
     const int gv = (int)((uint32_t)off / (uint32_t)nb), j = off - gv * nb;
     const int g = MULTI ? (int)((uint32_t)gv / (uint32_t)nrc) : gv;
+    const int flags = (j == 0 ? kInfoFirst : 0) | (j == nb - 1 ? kInfoLast : 0) | (pos == w0 ? kInfoStart : 0) |
+                      (pos == w1 - 1 ? kInfoEnd : 0) | (g << kInfoHeadShift) | (b << kInfoSeqShift);
+    if constexpr (PACK) {
+      const int b0 = s_ppre[b] >> 5, np = s_ppre[b] & 31, gs = p.group_size;
+      const int grp = b0 / gs, pp = s_gpp[grp];
+      int row, page, tok, act;
+      if (j < pp) {   // a prompt page: the group's first sequence names it
+        row = grp * gs;
+        page = j;
+        tok = kPage;
+        act = kActAll;
+      } else {
+        int jj = j - pp, m = 0;
+        while (m < np - 1) {
+          const int t = s_nfull[b0 + m] - pp;
+          if (jj < t) break;
+          jj -= t;
+          ++m;
+        }
+        row = b0 + m;
+        page = pp + jj;
+        tok = (page == s_nfull[row] - 1) ? s_tail[row] : kPage;
+        act = m;
+      }
+      c.pid = p.block_table[(int64_t)row * p.max_pages + page];
+      c.info = tok | flags | (act << kInfoActShift);
+      return c;
+    }
     const int tok = (j == nb - 1) ? s_tail[b] : (MULTI ? (j == nb - 2 ? min(kPage + s_tail[b], 31) : 31) : kPage);
     const int pp = MULTI ? 0 : s_ppre[b];   // prompt pages handled by the prompt pass (grouped runs)
     c.pid = p.block_table[(int64_t)b * p.max_pages + pp + j];
-    c.info = tok | (j == 0 ? kInfoFirst : 0) | (j == nb - 1 ? kInfoLast : 0) | (pos == w0 ? kInfoStart : 0) |
-             (pos == w1 - 1 ? kInfoEnd : 0) | (g << kInfoHeadShift) | (b << kInfoSeqShift) |
-             (MULTI ? (gv - g * nrc) << kInfoChunkShift : (pp > 0 ? kInfoPrompt : 0));
+    c.info = tok | flags | (MULTI ? (gv - g * nrc) << kInfoChunkShift : (pp > 0 ? kInfoPrompt : 0));
   }
   return c;
 }
@@ -678,17 +710,23 @@ __device__ __forceinline__ StreamChunk fetch_chunk(const Params& p, const int32_
 // rows per (sequence, KV head)): (b, g) has n_b * G rows, row r is query head
 // (r % G) of query row q_start[b] + r / G and sees keys below L - n_b + r / G + 1;
 // its rows are streamed as row_chunks segments of 16 rows each.
-template <class Pol, bool MULTI = false, int NT = 1>
+template <class Pol, bool MULTI = false, int NT = 1, bool PACK = false>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(1, 1)))
 void decode_attention_kernel(const Params p) {
   static_assert(NT == 1 || (MULTI && NT == 2), "two row tiles only for multi-token rows");
+  static_assert(!PACK || MULTI, "packed grouped runs use the multi-token row machinery");
   constexpr int D = Pol::kD;
   constexpr int DPT = D / 16;   // output elements per thread in the workgroup merge
-  __shared__ int32_t s_pre[kMaxBatch + 1];
-  __shared__ uint8_t s_tail[kMaxBatch];   // valid tokens of each sequence's last page
+  constexpr int kB = PACK ? kPackMaxBatch : kMaxBatch;
+  // Units: sequences, or packs of group members (packed grouped runs).
+  __shared__ int32_t s_pre[kB + 1];
+  __shared__ uint8_t s_tail[kB];   // valid tokens of each sequence's last page
   // Grouped runs: leading pages covered by the prompt pass.  Multi-token runs:
-  // (q_start[b] << 5) | n_b.
-  __shared__ int32_t s_ppre[kMaxBatch];
+  // (q_start[b] << 5) | n_b.  Packed grouped runs: (first member << 5) | members.
+  __shared__ int32_t s_ppre[kB];
+  // Packed grouped runs: pages of each sequence, and the clamped prompt pages of each group.
+  __shared__ uint16_t s_nfull[PACK ? kB : 1];
+  __shared__ int16_t s_gpp[PACK ? kB : 1];
   // Cut pieces: slot 2w holds wave w's piece that began before its quarter of the
   // share, slot 2w+1 its piece that continues past it.
   __shared__ __align__(16) float s_acc[2 * kWaves][16][D + 4];
@@ -713,13 +751,58 @@ void decode_attention_kernel(const Params p) {
   // sequence; a wave holds NT 16-row tiles against each page of a segment.
   const int nrc = MULTI ? p.row_chunks : 1, Hs = Hkv * nrc;
   constexpr int kSegRows = 16 * NT;
+  // The 16 NT-row chunk of its (sequence, KV head) that a page's segment covers.
+  auto chunk_of_info = [](int info) { return PACK ? 0 : (info >> kInfoChunkShift) & 3; };
 
-  // 1. Page counts per sequence and their prefix sums (identical in every workgroup).
+  // Units of the flattened list: sequences, or packs (packed grouped runs).
+  const int nunits = PACK ? p.pack_units : batch;
+  if constexpr (PACK) {
+    // Pages and last-page tokens of every sequence, then each group's prompt pages:
+    // the requested count clamped to the full pages of its shortest member.
+    int bad = 0;
+    for (int b = tid; b < batch; b += kThreads) {
+      int L = p.seq_lens[b];
+      if (L < 0 || L > cap) bad = 1;
+      L = min(max(L, 0), cap);
+      const int nf = (L + kPage - 1) / kPage;
+      s_nfull[b] = (uint16_t)nf;
+      s_tail[b] = (uint8_t)(L - (nf - 1) * kPage);
+    }
+    if (bad && u == 0) atomicOr(p.flags, kFlagBadLen);
+    __syncthreads();
+    const int gs = p.group_size, ngroups = (batch + gs - 1) / gs;
+    for (int i = tid; i < ngroups; i += kThreads) {
+      int mn = 0x7fffffff;
+      for (int b = i * gs; b < min(batch, (i + 1) * gs); ++b) {
+        const int nf = s_nfull[b];
+        mn = min(mn, (nf > 0 && s_tail[b] < kPage) ? nf - 1 : nf);   // full pages
+      }
+      const int want = p.prefix_pages[i], pp = max(0, min(want, mn));
+      if (want != pp && u == 0) atomicOr(p.flags, kFlagPrefixClamped);
+      s_gpp[i] = (int16_t)pp;
+    }
+    __syncthreads();
+  }
+
+  // 1. Page counts per unit and their prefix sums (identical in every workgroup).
   {
-    const int per = (batch + kThreads - 1) / kThreads;
-    const int lo = min(tid * per, batch), hi = min(lo + per, batch);
+    const int per = (nunits + kThreads - 1) / kThreads;
+    const int lo = min(tid * per, nunits), hi = min(lo + per, nunits);
     int sum = 0, bad = 0;
     for (int b = lo; b < hi; ++b) {
+      if constexpr (PACK) {
+        // Pack b: members b0 .. b0 + np - 1 of group i; the prompt once, then each member's own pages.
+        const int gs = p.group_size, P = p.pack, ppg = (gs + P - 1) / P;
+        const int i = b / ppg, r = b - i * ppg;
+        const int b0 = i * gs + r * P, np = min(P, min(batch, (i + 1) * gs) - b0);
+        const int pp = s_gpp[i];
+        int n = pp;
+        for (int m = 0; m < np; ++m) n += s_nfull[b0 + m] - pp;
+        s_ppre[b] = (b0 << 5) | np;
+        s_pre[b + 1] = n;
+        sum += n;
+        continue;
+      }
       int L = p.seq_lens[b];
       if (L < 0 || L > cap) bad = 1;
       L = min(max(L, 0), cap);
@@ -768,11 +851,11 @@ void decode_attention_kernel(const Params p) {
     if (tid == 0) s_pre[0] = 0;
     __syncthreads();
   }
-  const int64_t T = uni64((int64_t)s_pre[batch] * Hs);
+  const int64_t T = uni64((int64_t)s_pre[nunits] * Hs);
 
   // 2. Sequences with no pages left to stream: zero rows, or (grouped runs) the
   //    normalised prompt-pass result when the prompt is the whole sequence.
-  for (int b = u; b < batch; b += W) {
+  for (int b = u; b < nunits; b += W) {
     if (s_pre[b + 1] != s_pre[b]) continue;
     if constexpr (MULTI) {
       // Rows of a sequence with no keys (none, or rows claimed past an empty cache).
@@ -827,11 +910,13 @@ void decode_attention_kernel(const Params p) {
     QN qring[kDepth];
     typename Pol::PInit pring[kDepth];
     bool began = false;   // the segment being accumulated began inside this quarter
-    StreamChunk nxt = fetch_chunk<MULTI>(p, s_pre, s_tail, s_ppre, w0, w0, w1, lane, Hs, nrc);
+    StreamChunk nxt = fetch_chunk<MULTI, PACK>(p, s_pre, s_tail, s_ppre, s_nfull, s_gpp, nunits, w0, w0, w1, lane, Hs, nrc);
     for (int base = w0; base < w1; base += kChunk) {
       const StreamChunk cur = nxt;
       const int cn = min(kChunk, w1 - base);
-      if (base + kChunk < w1) nxt = fetch_chunk<MULTI>(p, s_pre, s_tail, s_ppre, base + kChunk, w0, w1, lane, Hs, nrc);
+      if (base + kChunk < w1)
+        nxt = fetch_chunk<MULTI, PACK>(p, s_pre, s_tail, s_ppre, s_nfull, s_gpp, nunits, base + kChunk, w0, w1, lane,
+                                       Hs, nrc);
       typename Pol::Frag fr[kDepth];
       int sinfo[kDepth];
       float skm[kDepth], svm[kDepth];
@@ -850,7 +935,7 @@ void decode_attention_kernel(const Params p) {
           }
         }
         const int tok = info & kInfoTok;
-        const int g = (info >> kInfoHeadShift) & 255, b = (info >> kInfoSeqShift) & 8191;
+        const int g = (info >> kInfoHeadShift) & 255, b = (info >> kInfoSeqShift) & (PACK ? 4095 : 8191);
         if constexpr (Pol::kFp8) {
           // Scales of (page, KV head); no records (reads of zero) for an absent page.
           const int64_t si = (pk >= 0) ? (int64_t)pk * Hkv + g : 0;
@@ -863,7 +948,7 @@ void decode_attention_kernel(const Params p) {
         const uint32_t nrec = ptok > 0 ? (uint32_t)((ptok - 1) * p.stride_slot + D * Pol::kEB) : 0u;
         st.issue(f, make_rsrc_uni((const char*)p.k + po, nrec), make_rsrc_uni((const char*)p.v + po, nrec));
         if constexpr (MULTI) {
-          const int qs = s_ppre[b], rb = kSegRows * ((info >> kInfoChunkShift) & 3);
+          const int qs = s_ppre[b], rb = kSegRows * chunk_of_info(info);
           const bool ld = (info & (kInfoFirst | kInfoStart)) != 0;
           Pol::load_q_multi(q_out.t[0], p, qs >> 5, qs & 31, g, rb, lane, ld);
           if constexpr (NT == 2) Pol::load_q_multi(q_out.t[NT - 1], p, qs >> 5, qs & 31, g, rb + 16, lane, ld);
@@ -879,7 +964,7 @@ void decode_attention_kernel(const Params p) {
       auto compute = [&](const typename Pol::Frag& f, int info, float km, float vm, const QN& q,
                          const typename Pol::PInit& pi, int k) {
         if (k >= cn) return;
-        const int g = (info >> kInfoHeadShift) & 255, b = (info >> kInfoSeqShift) & 8191;
+        const int g = (info >> kInfoHeadShift) & 255, b = (info >> kInfoSeqShift) & (PACK ? 4095 : 8191);
         if (info & (kInfoFirst | kInfoStart)) {
           bool seeded = false;
           if constexpr (Pol::kQRing && !MULTI) {
@@ -889,17 +974,31 @@ void decode_attention_kernel(const Params p) {
             }
           }
           if (!seeded) st.begin(q.t[0], p, b, g, lane);
-          if constexpr (MULTI) {
-            const int nq = s_ppre[b] & 31, r = kSegRows * ((info >> kInfoChunkShift) & 3) + (lane & 15);
+          if constexpr (MULTI && !PACK) {
+            const int nq = s_ppre[b] & 31, r = kSegRows * chunk_of_info(info) + (lane & 15);
             st.shift = (r < nq * G) ? nq - 1 - r / G : 0;
             if constexpr (NT == 2) {
               st2.begin(q.t[NT - 1], p, b, g, lane);
               st2.shift = (r + 16 < nq * G) ? nq - 1 - (r + 16) / G : 0;
             }
           }
+          if constexpr (PACK) {
+            if constexpr (NT == 2) st2.begin(q.t[NT - 1], p, b, g, lane);
+          }
           began = (info & kInfoFirst) != 0;
         }
-        if constexpr (MULTI) {
+        if constexpr (PACK) {
+          // A member's own page counts for its rows only; a prompt page for every row.
+          const int act = (info >> kInfoActShift) & 7, tok = info & kInfoTok, r = lane & 15;
+          // A tile none of whose rows the page serves is skipped (its state would not change).
+          if (NT == 1 || act == kActAll || act * G < 16)
+            st.template compute<true>(f, lane, (act == kActAll || r / G == act) ? tok : 0, p.scale_log2 * km, vm);
+          if constexpr (NT == 2) {
+            if (act == kActAll || (act + 1) * G > 16)
+              st2.template compute<true>(f, lane, (act == kActAll || (16 + r) / G == act) ? tok : 0,
+                                         p.scale_log2 * km, vm);
+          }
+        } else if constexpr (MULTI) {
           st.template compute<true>(f, lane, info & kInfoTok, p.scale_log2 * km, vm);
           if constexpr (NT == 2) st2.template compute<true>(f, lane, info & kInfoTok, p.scale_log2 * km, vm);
         } else
@@ -908,7 +1007,7 @@ void decode_attention_kernel(const Params p) {
           const bool ended = (info & kInfoLast) != 0;
           if (began && ended) {
             if constexpr (MULTI) {
-              const int rb = kSegRows * ((info >> kInfoChunkShift) & 3);
+              const int rb = kSegRows * chunk_of_info(info);
               st.write_out_multi(p, s_ppre[b] >> 5, s_ppre[b] & 31, g, rb, lane);
               if constexpr (NT == 2) st2.write_out_multi(p, s_ppre[b] >> 5, s_ppre[b] & 31, g, rb + 16, lane);
             } else {
@@ -920,7 +1019,7 @@ void decode_attention_kernel(const Params p) {
             if constexpr (NT == 2) {
               if (ended) held = st2;   // slot 2w+1 is the quarter's last piece: st2 keeps it
             }
-            if (lane == 0) s_seg[slot] = b * Hs + (MULTI ? g * nrc + ((info >> kInfoChunkShift) & 3) : g);
+            if (lane == 0) s_seg[slot] = b * Hs + (MULTI ? g * nrc + chunk_of_info(info) : g);
           }
         }
       };
@@ -1350,11 +1449,11 @@ int launch_append_t(const Params& p, void* stream) {
   return (int)hipGetLastError();
 }
 
-template <class Pol, bool MULTI = false, int NT = 1>
+template <class Pol, bool MULTI = false, int NT = 1, bool PACK = false>
 int launch(const Params& p, void* stream, void* ev_begin, void* ev_end) {
   hipStream_t st = (hipStream_t)stream;
   if (ev_begin && hipEventRecord((hipEvent_t)ev_begin, st) != hipSuccess) return -1;
-  hipLaunchKernelGGL((decode_attention_kernel<Pol, MULTI, NT>), dim3(p.nranges), dim3(kThreads), 0, st, p);
+  hipLaunchKernelGGL((decode_attention_kernel<Pol, MULTI, NT, PACK>), dim3(p.nranges), dim3(kThreads), 0, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
   if (ev_end && hipEventRecord((hipEvent_t)ev_end, st) != hipSuccess) return -1;
@@ -1398,6 +1497,12 @@ int launch_rows(int tiles, const Params& p, void* stream, void* ev_begin, void* 
   return tiles == 2 ? launch<Pol, true, 2>(p, stream, ev_begin, ev_end) : launch<Pol, true, 1>(p, stream, ev_begin, ev_end);
 }
 
+template <class Pol>
+int launch_packed(int tiles, const Params& p, void* stream, void* ev_begin, void* ev_end) {
+  return tiles == 2 ? launch<Pol, true, 2, true>(p, stream, ev_begin, ev_end)
+                    : launch<Pol, true, 1, true>(p, stream, ev_begin, ev_end);
+}
+
 int launch_decode_rows(KvKind kind, int head_dim, int tiles, const Params& p, void* stream, void* ev_begin,
                        void* ev_end) {
   switch (kind) {
@@ -1407,6 +1512,21 @@ int launch_decode_rows(KvKind kind, int head_dim, int tiles, const Params& p, vo
     case KvKind::FP8:
       return head_dim == 128 ? launch_rows<Mfma<128, true>>(tiles, p, stream, ev_begin, ev_end)
                              : launch_rows<Mfma<64, true>>(tiles, p, stream, ev_begin, ev_end);
+    case KvKind::F32:
+      break;
+  }
+  return -1;
+}
+
+int launch_decode_packed(KvKind kind, int head_dim, int tiles, const Params& p, void* stream, void* ev_begin,
+                         void* ev_end) {
+  switch (kind) {
+    case KvKind::BF16:
+      return head_dim == 128 ? launch_packed<Mfma<128, false>>(tiles, p, stream, ev_begin, ev_end)
+                             : launch_packed<Mfma<64, false>>(tiles, p, stream, ev_begin, ev_end);
+    case KvKind::FP8:
+      return head_dim == 128 ? launch_packed<Mfma<128, true>>(tiles, p, stream, ev_begin, ev_end)
+                             : launch_packed<Mfma<64, true>>(tiles, p, stream, ev_begin, ev_end);
     case KvKind::F32:
       break;
   }

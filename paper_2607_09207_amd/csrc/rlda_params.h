@@ -60,6 +60,8 @@ struct Params {
   int32_t pfx_nblocks;         // jobs per (group, KV head)
   int32_t pfx_splits;          // workgroups per job (their states meet in the partial slots)
   int32_t pfx_slots;           // capacity of part_acc / part_ml in 64-row prompt-pass slots
+  int32_t pack;                // packed grouped runs: members per pack (their rows share the MFMA tiles)
+  int32_t pack_units;          // packed grouped runs: packs in the batch
   // KV append (rl_decode_attn_append): the step's new rows, [batch][Hkv][D] in the q dtype.
   const void* k_in;
   const void* v_in;
@@ -89,11 +91,23 @@ int launch_multi(KvKind kind, int head_dim, const Params& p, int grid, void* str
 // (tiles 1 or 2): the decode kernel's page stream, each row masked causally (bf16 / fp8).
 int launch_decode_rows(KvKind kind, int head_dim, int tiles, const Params& p, void* stream, void* ev_begin,
                        void* ev_end);
+// Grouped runs with the members of a group packed into the rows of the MFMA tiles
+// (pack members per (pack, KV head) segment): the decode kernel's page stream, the
+// prompt pages streamed once per pack, each member's own pages after them.
+int launch_decode_packed(KvKind kind, int head_dim, int tiles, const Params& p, void* stream, void* ev_begin,
+                         void* ev_end);
 #ifndef RLDA_MQ_TILES
 #define RLDA_MQ_TILES 1            // 32-row MFMA tiles per wave in the multi-token kernel
 #endif
 constexpr int kMultiTiles = RLDA_MQ_TILES;
 constexpr int kMultiRows = 128 * kMultiTiles;   // query rows (token, head pairs) per workgroup of the multi-token kernel
 constexpr int kMultiMaxBatch = 4096;   // its per-sequence LDS table stays within 64 KiB of LDS per workgroup
+constexpr int kPackMaxBatch = 4096;    // packed grouped runs: per-sequence and per-pack LDS tables of this size
+constexpr int kPackMaxMembers = 7;     // ... members per pack (3 bits of the page descriptor, 7 = every member)
+constexpr int kPackMaxPages = 32767;   // ... pages per sequence (16-bit LDS entries)
+#ifndef RLDA_PACK_TILES
+#define RLDA_PACK_TILES 1          // 16-row tiles a wave holds per pack (1 or 2)
+#endif
+constexpr int kPackTiles = RLDA_PACK_TILES;
 
 }  // namespace rlda

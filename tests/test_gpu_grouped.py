@@ -93,13 +93,30 @@ def test_partial_claims_and_uneven_groups(torch_cuda):
     assert_close(got, oracle.run(w), "bf16", "uneven")
 
 
-def test_zero_prompt_is_bitwise_the_plain_run(torch_cuda):
+def test_zero_prompt_is_bitwise_the_plain_run_on_the_prompt_pass_path(torch_cuda):
+    # G = 16: no two members fit one tile, so the call runs the prompt pass and then
+    # the attention kernel, which with no prompt pages streams exactly what the plain
+    # call streams.
+    w = grouped_case(16, 1, 128, 4, 160, [33, 0, 700, 16])
+    t = I.to_torch(w, "cuda")
+    h = handle_for(w)
+    plain = h(t["q"], t["k_cache"], t["v_cache"], t["block_table"], t["seq_lens"]).cpu().numpy()
+    got, _ = run_grouped(torch_cuda, w, 4, [0], handle=h, tag="zero-prompt G=16")
+    assert np.array_equal(got.astype(np.float32).view(np.uint32), plain.view(np.uint32))
+
+
+def test_zero_prompt_on_the_packed_path_is_the_plain_result(torch_cuda):
+    # G = 7: two members share a tile; with no prompt pages a pack streams member 0's
+    # pages and then member 1's, each with only its rows unmasked.  Same values as the
+    # plain call up to the summation order of the split pieces.
     w = grouped_case(28, 4, 128, 4, 160, [33, 0, 700, 16])
     t = I.to_torch(w, "cuda")
     h = handle_for(w)
     plain = h(t["q"], t["k_cache"], t["v_cache"], t["block_table"], t["seq_lens"]).cpu().numpy()
-    got, _ = run_grouped(torch_cuda, w, 4, [0], handle=h, tag="zero-prompt")
-    assert np.array_equal(got.astype(np.float32).view(np.uint32), plain.view(np.uint32))
+    got, flags = run_grouped(torch_cuda, w, 4, [0], handle=h, tag="zero-prompt G=7")
+    assert flags == 0
+    assert_close(got, oracle.run(w), "bf16", "zero prompt packed")
+    assert np.max(np.abs(got - plain)) < 1e-5
 
 
 def test_other_members_prompt_entries_are_not_read(torch_cuda):
@@ -143,3 +160,25 @@ def test_grpo_workload_full_size_grouped(torch_cuda):
     want = oracle.run(w, batch_mask=mask)
     rows = np.nonzero(mask)[0]
     assert_close(got[rows], want[rows], "bf16", "grpo full grouped")
+
+
+def test_grouped_beyond_the_packed_batch_limit(torch_cuda):
+    # 4104 sequences (groups of 8, G = 6): past the packed path's 4096, so the call
+    # runs the prompt pass and the attention kernel; the result is the same operation.
+    rng = np.random.default_rng(83)
+    tails = rng.integers(0, 40, size=4104).tolist()
+    w = grouped_case(12, 2, 128, 8, 32, tails, seed=84, max_pages=6)
+    ng = (w.batch + 7) // 8
+    got, flags = run_grouped(torch_cuda, w, 8, [2] * ng, tag="beyond packed batch")
+    assert flags == 0
+    assert_close(got, oracle.run(w), "bf16", "grouped batch 4104")
+
+
+def test_packed_groups_with_empty_members_and_a_short_last_group(torch_cuda):
+    # G = 4: packs of 4 members; empty sequences inside packs; the call groups by 6,
+    # so the last group has 3 members (one pack of 3).
+    w = grouped_case(16, 4, 128, 5, 0, [0, 0, 33, 5, 0, 700, 16, 0, 1, 2, 0, 90, 0, 0, 300])
+    ng = (w.batch + 5) // 6
+    got, flags = run_grouped(torch_cuda, w, 6, [0] * ng, tag="packed empties")
+    assert flags == 0
+    assert_close(got, oracle.run(w), "bf16", "packed with empty members")
