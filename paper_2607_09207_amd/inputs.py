@@ -382,9 +382,21 @@ def verify_gqa_bf16(seed=1007, rows=4):
     return with_query_rows(w, np.minimum(lens, rows))
 
 
+def chunked_prefill_fp8(seed=1008, chunk=512):
+    """Chunked prefill on an fp8-e4m3fn cache shaped like the fp8 workload: 64
+    sequences, 40 query / 8 KV heads, d=128, one fp32 scale per (page, KV head), q
+    bf16, total lengths lognormal (median 4096, sigma 1.0) clipped to [64, 32768];
+    each sequence's last min(chunk, L) tokens are the chunk's query rows."""
+    rng = np.random.default_rng(seed)
+    lens = _lognormal_lengths(rng, 64, 4096, 1.0, 64, 32768)
+    w = _scattered("chunked_prefill_fp8", seed, rng, lens, 40, 8, 128, "bf16", "fp8_e4m3fn", 2048)
+    return with_query_rows(w, np.minimum(lens, chunk))
+
+
 MULTI_WORKLOADS = {
     "prompt_prefill_grpo_bf16": prompt_prefill_grpo_bf16,
     "chunked_prefill_gqa_bf16": chunked_prefill_gqa_bf16,
+    "chunked_prefill_fp8": chunked_prefill_fp8,
     "verify_gqa_bf16": verify_gqa_bf16,
 }
 

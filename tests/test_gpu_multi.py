@@ -117,7 +117,7 @@ def test_inconsistent_offsets_flag_and_leave_their_rows_alone(torch_cuda):
 
 
 def test_full_size_prefill_workloads_sampled(torch_cuda):
-    for name in ("prompt_prefill_grpo_bf16", "chunked_prefill_gqa_bf16"):
+    for name in ("prompt_prefill_grpo_bf16", "chunked_prefill_gqa_bf16", "chunked_prefill_fp8"):
         w = I.make_workload(name)
         got, flags = run_multi(torch_cuda, w, tag=name)
         assert flags == 0
@@ -128,7 +128,7 @@ def test_full_size_prefill_workloads_sampled(torch_cuda):
         mask[pick] = 1
         want = oracle.run_multi(w, batch_mask=mask)
         rows = np.concatenate([np.arange(w.q_start[b], w.q_start[b + 1]) for b in pick])
-        assert_close(got[rows], want[rows], "bf16", f"{name} sampled sequences {pick}")
+        assert_close(got[rows], want[rows], w.kv_dtype, f"{name} sampled sequences {pick}")
 
 
 def test_multi_is_bitwise_deterministic(torch_cuda):

@@ -169,3 +169,19 @@ def test_h_dec_equals_sum_over_decode_steps():
     brute = sum(int(pi) + t - 1 for pi, ri in zip(p, r) for t in range(1, int(ri) + 1))
     assert A.h_dec(p, r) == brute
     assert A.b_kv(28, 4, 128, 2, tp=2) == 2 * 28 * 4 * 128 * 2 / 2
+
+
+@pytest.mark.parametrize("name,heads,kv,rows_per_seq", [
+    ("prompt_prefill_grpo_bf16", (12, 2), "bf16", None),        # whole 512-token prompts
+    ("chunked_prefill_gqa_bf16", (28, 4), "bf16", 512),
+    ("chunked_prefill_fp8", (40, 8), "fp8_e4m3fn", 512),
+    ("verify_gqa_bf16", (28, 4), "bf16", 4),
+])
+def test_multi_token_workloads_take_the_last_tokens_as_query_rows(name, heads, kv, rows_per_seq):
+    w = I.make_workload(name)
+    assert (w.num_q_heads, w.num_kv_heads, w.head_dim, w.q_dtype, w.kv_dtype) == (*heads, 128, "bf16", kv)
+    ql = np.diff(np.asarray(w.q_start))
+    assert w.q_start[0] == 0 and w.q.shape[0] == int(w.q_start[-1])
+    want = w.seq_lens if rows_per_seq is None else np.minimum(w.seq_lens, rows_per_seq)
+    assert np.array_equal(ql, want)
+    _check_table(w)
