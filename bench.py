@@ -330,7 +330,7 @@ def main():
         if not (w.shared_prefix_tokens > 0 and w.group_size > 1):
             raise SystemExit(f"--grouped on: workload {w.name} has no shared prompt")
         ng = (w.batch + w.group_size - 1) // w.group_size
-        gkw = dict(group_size=w.group_size,
+        gkw = dict(group_size=w.group_size, prompt_pages_hint=w.shared_prefix_tokens // w.page_size,
                    prefix_pages=torch.full((ng,), w.shared_prefix_tokens // w.page_size, dtype=torch.int32, device=dev))
     ws = h.workspace(dev, grouped=grouped)
     stream = torch.cuda.current_stream(dev)

@@ -144,7 +144,9 @@ rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t handle, int32_t batch, 
  * result is that of rl_decode_attn_run on the same arguments (up to rounding
  * order), but prompt pages are read fewer times.  Two ways, chosen on the host:
  *   - packed (at least two members fit the 16 rows of one MFMA tile: 2G <= 16,
- *     group_size >= 2, batch <= 4096, max_pages_per_seq <= 32767): one kernel.
+ *     group_size >= 2, batch <= 4096, max_pages_per_seq <= 32767, and the prompt
+ *     bytes packing reads again, (packs per group - 1) * groups * Hkv *
+ *     prompt_pages_hint * 32 * head_dim * bytes(kv), below 200 MiB): one kernel.
  *     Up to min(7, 16/G) consecutive members of a group form a pack whose rows
  *     share one tile; the pack's segment streams the prompt pages once with every
  *     member's rows, then each member's own pages with only its rows unmasked.
@@ -156,6 +158,9 @@ rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t handle, int32_t batch, 
  *     and KV head.
  *   group_size    >= 1, host value
  *   prefix_pages  [ceil(batch / group_size)] int32, device memory
+ *   prompt_pages_hint  host value: the caller's estimate of the prompt pages (e.g. the
+ *                 largest prefix_pages entry); only chooses between the two ways;
+ *                 <= 0: unknown (packed when the other conditions hold)
  * The prompt pages are read from the block-table row of the group's first
  * sequence; the other members' first prefix_pages[i] entries are not read (a
  * member whose entries differ is computed as if they matched).  A group's prompt
@@ -170,8 +175,9 @@ rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t handle, int32_t batch, 
  * recorded before the first and after the last kernel.
  */
 rlda_status rl_decode_attn_run_grouped(rl_decode_attn_t handle, int32_t batch, int32_t num_pages, int32_t group_size,
-                                       const int32_t* prefix_pages, const void* q, const void* k_cache,
-                                       const void* v_cache, const float* k_scale, const float* v_scale,
+                                       const int32_t* prefix_pages, int32_t prompt_pages_hint, const void* q,
+                                       const void* k_cache, const void* v_cache, const float* k_scale,
+                                       const float* v_scale,
                                        const int32_t* block_table, const int32_t* seq_lens, void* out,
                                        void* workspace, size_t workspace_bytes, void* stream, void* event_begin,
                                        void* event_end);

@@ -105,12 +105,14 @@ class DecodeAttention:
 
     def __call__(self, q, k_cache, v_cache, block_table, seq_lens, k_scale=None, v_scale=None, out=None,
                  workspace=None, stream=None, num_pages: Optional[int] = None, events=None,
-                 group_size: Optional[int] = None, prefix_pages=None):
+                 group_size: Optional[int] = None, prefix_pages=None, prompt_pages_hint: int = -1):
         """Queue the attention on `stream` (default: the current stream).  With
         events=(begin, end) (torch.cuda.Event, timing enabled) the two events bracket
         the library's kernels.  With group_size and prefix_pages (int32 device tensor,
         one entry per group of group_size consecutive sequences) the call shares each
-        group's prompt pages (rl_decode_attn_run_grouped)."""
+        group's prompt pages (rl_decode_attn_run_grouped); prompt_pages_hint (host value,
+        e.g. the largest prefix_pages entry, <= 0 unknown) picks its packed or
+        prompt-pass form."""
         torch = _torch()
         B = int(q.shape[0])
         cfg = self.config
@@ -130,7 +132,7 @@ class DecodeAttention:
                 ptr(block_table), ptr(seq_lens), ptr(out), wp, ws.numel() - (wp - ws.data_ptr()), stream)
         if grouped:
             e0, e1 = (None, None) if events is None else tuple(self._event_handle(e) for e in events)
-            gargs = args[:3] + (int(group_size), ptr(prefix_pages)) + args[3:] + (e0, e1)
+            gargs = args[:3] + (int(group_size), ptr(prefix_pages), int(prompt_pages_hint)) + args[3:] + (e0, e1)
             _abi.check(self._lib.rl_decode_attn_run_grouped(*gargs), "rl_decode_attn_run_grouped")
         elif events is None:
             _abi.check(self._lib.rl_decode_attn_run(*args), "rl_decode_attn_run")
@@ -144,8 +146,8 @@ class DecodeAttention:
         """Multi-token queries (rl_decode_attn_run_multi): q [total_q][Hq][d], q_start
         [batch + 1] int32 device tensor; sequence b's rows q[q_start[b]:q_start[b+1]]
         are its last tokens and attend causally.  max_q_len (host value) bounds the
-        rows per sequence; with max_q_len * G <= 16 the decode kernel's page stream
-        runs the call.  Returns out [total_q][Hq][d]."""
+        rows per sequence; with max_q_len <= 16 and max_q_len * G <= 64 the decode
+        kernel's page stream runs the call.  Returns out [total_q][Hq][d]."""
         torch = _torch()
         total = int(q.shape[0])
         B = int(q_start.shape[0]) - 1

@@ -63,7 +63,7 @@ def load() -> ctypes.CDLL:
         lib.rl_decode_attn_run.restype = ctypes.c_int
         lib.rl_decode_attn_run_profiled.argtypes = [vp, i32, i32] + [vp] * 8 + [vp, sz, vp, vp, vp]
         lib.rl_decode_attn_run_profiled.restype = ctypes.c_int
-        lib.rl_decode_attn_run_grouped.argtypes = [vp, i32, i32, i32, vp] + [vp] * 8 + [vp, sz, vp, vp, vp]
+        lib.rl_decode_attn_run_grouped.argtypes = [vp, i32, i32, i32, vp, i32] + [vp] * 8 + [vp, sz, vp, vp, vp]
         lib.rl_decode_attn_run_grouped.restype = ctypes.c_int
         lib.rl_decode_attn_grouped_workspace_size.argtypes = [vp, ctypes.POINTER(sz)]
         lib.rl_decode_attn_grouped_workspace_size.restype = ctypes.c_int

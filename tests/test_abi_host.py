@@ -165,7 +165,7 @@ def test_grouped_run_rejects_bad_arguments_before_launch(lib):
     f = 0x10000
 
     def run(batch=8, gs=4, pp=f, wsb=None, e0=None, e1=None, handle=h):
-        return lib.rl_decode_attn_run_grouped(handle, batch, 10, gs, pp, f, f, f, None, None, f, f, f, f * 16,
+        return lib.rl_decode_attn_run_grouped(handle, batch, 10, gs, pp, -1, f, f, f, None, None, f, f, f, f * 16,
                                               ng.value if wsb is None else wsb, None, e0, e1)
 
     assert run(gs=0) == -1                # group size must be >= 1

@@ -24,14 +24,15 @@ def torch_cuda():
     return torch
 
 
-def run_grouped(torch, w, group_size, prefix_pages, out_dtype="f32", ranges=0, tag="", handle=None, ws=None):
+def run_grouped(torch, w, group_size, prefix_pages, out_dtype="f32", ranges=0, tag="", handle=None, ws=None,
+                hint=-1):
     log(f"{tag} grouped B={w.batch} Hq={w.num_q_heads} Hkv={w.num_kv_heads} d={w.head_dim} kv={w.kv_dtype} "
-        f"group={group_size} prefix_pages={list(prefix_pages)[:6]} ranges={ranges} out={out_dtype}")
+        f"group={group_size} prefix_pages={list(prefix_pages)[:6]} ranges={ranges} out={out_dtype} hint={hint}")
     t = I.to_torch(w, "cuda")
     h = handle or handle_for(w, out_dtype, ranges)
     pp = torch.tensor(np.asarray(prefix_pages, np.int32), device="cuda")
     out = h(t["q"], t["k_cache"], t["v_cache"], t["block_table"], t["seq_lens"], k_scale=t["k_scale"],
-            v_scale=t["v_scale"], group_size=group_size, prefix_pages=pp, workspace=ws)
+            v_scale=t["v_scale"], group_size=group_size, prefix_pages=pp, workspace=ws, prompt_pages_hint=hint)
     torch.cuda.synchronize()
     flags = h.read_flags(workspace=ws, device=out.device)
     return out.float().cpu().numpy().astype(np.float64), flags
@@ -182,3 +183,13 @@ def test_packed_groups_with_empty_members_and_a_short_last_group(torch_cuda):
     got, flags = run_grouped(torch_cuda, w, 6, [0] * ng, tag="packed empties")
     assert flags == 0
     assert_close(got, oracle.run(w), "bf16", "packed with empty members")
+
+
+@pytest.mark.parametrize("hint", [-1, 32, 100000])
+def test_prompt_length_hint_only_chooses_the_form(torch_cuda, hint):
+    # G = 6, groups of 8: packed for unknown or short prompts, the prompt pass for a
+    # long one; the values are the operation's either way.
+    w = grouped_case(12, 2, 128, 8, 512, [0, 1, 15, 16, 17, 300, 2000, 5] * 2)
+    got, flags = run_grouped(torch_cuda, w, 8, [32, 32], hint=hint, tag=f"hint={hint}")
+    assert flags == 0
+    assert_close(got, oracle.run(w), "bf16", f"grouped hint={hint}")
