@@ -39,6 +39,10 @@
 // fp8 (OCP E4M3FN) caches are converted exactly to bf16 for the MFMA; the K
 // scale multiplies the scores and the V scale multiplies P.  fp32 caches use a
 // VALU path.
+// The same kernel serves multi-token rows (a few query rows per sequence, each
+// masked at its causal position, up to two 16-row tiles per wave) and packed
+// GRPO groups (the members of a group in the rows of one tile, the shared prompt
+// pages streamed once per pack); see decode_attention_kernel.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -706,10 +710,15 @@ __device__ __forceinline__ StreamChunk fetch_chunk(const Params& p, const int32_
 
 // ---------------------------------------------------------------- the kernel
 
-// MULTI: multi-token rows (rl_decode_attn_run_multi with at most 16 * row_chunks
+// MULTI: multi-token rows (rl_decode_attn_run_multi with at most 16 NT row_chunks
 // rows per (sequence, KV head)): (b, g) has n_b * G rows, row r is query head
 // (r % G) of query row q_start[b] + r / G and sees keys below L - n_b + r / G + 1;
-// its rows are streamed as row_chunks segments of 16 rows each.
+// its rows are streamed as row_chunks segments of 16 NT rows, NT tiles of 16 rows
+// per wave against each page.
+// PACK (with MULTI): grouped runs with the members of a GRPO group packed into
+// the rows of the tiles.  The units are packs instead of sequences; row r of a
+// pack is query head (r % G) of member r / G, and a page counts for every row (a
+// prompt page) or for one member's rows (its own pages).
 template <class Pol, bool MULTI = false, int NT = 1, bool PACK = false>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(1, 1)))
 void decode_attention_kernel(const Params p) {
