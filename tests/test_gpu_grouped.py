@@ -193,3 +193,15 @@ def test_prompt_length_hint_only_chooses_the_form(torch_cuda, hint):
     got, flags = run_grouped(torch_cuda, w, 8, [32, 32], hint=hint, tag=f"hint={hint}")
     assert flags == 0
     assert_close(got, oracle.run(w), "bf16", f"grouped hint={hint}")
+
+
+@pytest.mark.parametrize("kv", ["bf16", "fp8_e4m3fn"])
+def test_grouped_strided_layout(torch_cuda, kv):
+    # [page][slot][head][d] pool viewed through strides, packed (G = 6) and prompt-pass
+    # (hint past the packing threshold) forms
+    w = I.to_page_slot_head(grouped_case(12, 2, 128, 4, 256, [0, 9, 400, 33, 70, 1, 16, 5], kv=kv, seed=11))
+    ng = (w.batch + 3) // 4
+    for hint in (-1, 1 << 20):
+        got, flags = run_grouped(torch_cuda, w, 4, [16] * ng, hint=hint, tag=f"strided {kv} hint={hint}")
+        assert flags == 0
+        assert_close(got, oracle.run(w), kv, f"grouped strided {kv} hint={hint}")
