@@ -281,7 +281,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (this path needs no "
-              "collectives and shards by sequence or KV head, see DESIGN.md)", file=sys.stderr)
+              "collectives; it shards by sequence or by KV head)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
