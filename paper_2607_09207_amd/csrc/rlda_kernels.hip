@@ -375,10 +375,54 @@ struct Mfma {
     }
   }
 
+  // V^T operands of a page for the 16x16x16 products, one per 16-wide output tile:
+  // lane 16q + i supplies V[rows 4q..4q+3][column D/16*i + t] of tile t (fp8
+  // converted exactly to bf16).  They depend on the page only, so the tiles of a
+  // wave that holds two share them.
+  struct VOp {
+    s16x4 a[DT];
+  };
+  __device__ __forceinline__ static VOp v_operand(const Frag& f) {
+    VOp vo;
+    if constexpr (!FP8) {
+#pragma unroll
+      for (int t = 0; t < DT; ++t) {
+        const uint32_t w0 = word_of(f.v[0], t >> 1), w1 = word_of(f.v[1], t >> 1);
+        const uint32_t w2 = word_of(f.v[2], t >> 1), w3 = word_of(f.v[3], t >> 1);
+        uint32_t lo, hi;
+        if ((t & 1) == 0) {
+          lo = (w0 & 0xFFFFu) | (w1 << 16);
+          hi = (w2 & 0xFFFFu) | (w3 << 16);
+        } else {
+          lo = (w0 >> 16) | (w1 & 0xFFFF0000u);
+          hi = (w2 >> 16) | (w3 & 0xFFFF0000u);
+        }
+        vo.a[t] = __builtin_bit_cast(s16x4, u32x2{lo, hi});
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < DT / 2; ++u) {   // element pair (2u, 2u+1) of each row
+        f32x2 c[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) c[r] = fp8x2_to_f32(word_of(f.v[r], u >> 1), (u & 1) != 0);
+#pragma unroll
+        for (int e = 0; e < 2; ++e)
+          vo.a[2 * u + e] = __builtin_bit_cast(s16x4, u32x2{pack_bf16(c[0][e], c[1][e]), pack_bf16(c[2][e], c[3][e])});
+      }
+    }
+    return vo;
+  }
+
   // Page with index `j` in its sequence; `valid_tokens` tokens of it count (for
   // multi-token rows: tokens of the page and after it, up to 31, less `shift`).
   template <bool MULTI = false>
   __device__ __forceinline__ void compute(const Frag& f, int lane, int valid_tokens, float kmul, float vmul) {
+    compute_with<MULTI>(f, nullptr, lane, valid_tokens, kmul, vmul);
+  }
+  // ... with the page's V operands built once by the caller (vo), or here (null).
+  template <bool MULTI = false>
+  __device__ __forceinline__ void compute_with(const Frag& f, const VOp* vo, int lane, int valid_tokens, float kmul,
+                                               float vmul) {
     const int qg = lane >> 4;
     f32x4 sc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -420,36 +464,9 @@ struct Mfma {
     l += ps;
     u32x2 pb2 = {pack_bf16(pr[0] * vmul, pr[1] * vmul), pack_bf16(pr[2] * vmul, pr[3] * vmul)};
     const s16x4 pb = __builtin_bit_cast(s16x4, pb2);
-    if constexpr (!FP8) {
+    const VOp v = vo ? *vo : v_operand(f);
 #pragma unroll
-      for (int t = 0; t < DT; ++t) {
-        const uint32_t w0 = word_of(f.v[0], t >> 1), w1 = word_of(f.v[1], t >> 1);
-        const uint32_t w2 = word_of(f.v[2], t >> 1), w3 = word_of(f.v[3], t >> 1);
-        uint32_t lo, hi;
-        if ((t & 1) == 0) {
-          lo = (w0 & 0xFFFFu) | (w1 << 16);
-          hi = (w2 & 0xFFFFu) | (w3 << 16);
-        } else {
-          lo = (w0 >> 16) | (w1 & 0xFFFF0000u);
-          hi = (w2 >> 16) | (w3 & 0xFFFF0000u);
-        }
-        u32x2 a2 = {lo, hi};
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a2), pb, acc[t], 0, 0, 0);
-      }
-    } else {
-#pragma unroll
-      for (int u = 0; u < DT / 2; ++u) {   // element pair (2u, 2u+1) of each row
-        f32x2 c[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) c[r] = fp8x2_to_f32(word_of(f.v[r], u >> 1), (u & 1) != 0);
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          u32x2 a2 = {pack_bf16(c[0][e], c[1][e]), pack_bf16(c[2][e], c[3][e])};
-          acc[2 * u + e] =
-              __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a2), pb, acc[2 * u + e], 0, 0, 0);
-        }
-      }
-    }
+    for (int t = 0; t < DT; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(v.a[t], pb, acc[t], 0, 0, 0);
   }
 
   // Write this wave's state in canonical [head][d] form to LDS.
@@ -1000,16 +1017,25 @@ void decode_attention_kernel(const Params p) {
           // A member's own page counts for its rows only; a prompt page for every row.
           const int act = (info >> kInfoActShift) & 7, tok = info & kInfoTok, r = lane & 15;
           // A tile none of whose rows the page serves is skipped (its state would not change).
-          if (NT == 1 || act == kActAll || act * G < 16)
+          if constexpr (NT == 1) {
             st.template compute<true>(f, lane, (act == kActAll || r / G == act) ? tok : 0, p.scale_log2 * km, vm);
-          if constexpr (NT == 2) {
+          } else {
+            const typename Pol::VOp vo = Pol::v_operand(f);
+            if (act == kActAll || act * G < 16)
+              st.template compute_with<true>(f, &vo, lane, (act == kActAll || r / G == act) ? tok : 0,
+                                             p.scale_log2 * km, vm);
             if (act == kActAll || (act + 1) * G > 16)
-              st2.template compute<true>(f, lane, (act == kActAll || (16 + r) / G == act) ? tok : 0,
-                                         p.scale_log2 * km, vm);
+              st2.template compute_with<true>(f, &vo, lane, (act == kActAll || (16 + r) / G == act) ? tok : 0,
+                                              p.scale_log2 * km, vm);
           }
         } else if constexpr (MULTI) {
-          st.template compute<true>(f, lane, info & kInfoTok, p.scale_log2 * km, vm);
-          if constexpr (NT == 2) st2.template compute<true>(f, lane, info & kInfoTok, p.scale_log2 * km, vm);
+          if constexpr (NT == 1) {
+            st.template compute<true>(f, lane, info & kInfoTok, p.scale_log2 * km, vm);
+          } else {
+            const typename Pol::VOp vo = Pol::v_operand(f);
+            st.template compute_with<true>(f, &vo, lane, info & kInfoTok, p.scale_log2 * km, vm);
+            st2.template compute_with<true>(f, &vo, lane, info & kInfoTok, p.scale_log2 * km, vm);
+          }
         } else
           st.compute(f, lane, info & kInfoTok, p.scale_log2 * km, vm);
         if (info & (kInfoLast | kInfoEnd)) {
