@@ -205,3 +205,13 @@ def test_grouped_strided_layout(torch_cuda, kv):
         got, flags = run_grouped(torch_cuda, w, 4, [16] * ng, hint=hint, tag=f"strided {kv} hint={hint}")
         assert flags == 0
         assert_close(got, oracle.run(w), kv, f"grouped strided {kv} hint={hint}")
+
+
+def test_packed_path_at_its_largest_batch(torch_cuda):
+    # 4096 sequences in groups of 8 (G = 6, packs of 2): the packed path's limit.
+    rng = np.random.default_rng(85)
+    tails = rng.integers(0, 40, size=4096).tolist()
+    w = grouped_case(12, 2, 128, 8, 32, tails, seed=86, max_pages=6)
+    got, flags = run_grouped(torch_cuda, w, 8, [2] * (4096 // 8), tag="packed batch 4096")
+    assert flags == 0
+    assert_close(got, oracle.run(w), "bf16", "packed batch 4096")
