@@ -242,11 +242,11 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32
   }
   p.prefix_pages = prefix_pages;
   p.group_size = group_size;
-  // Packed: up to 16 * tiles / G members of a group share the rows of the MFMA
-  // tiles, so one segment streams the prompt pages once for all of them and then
-  // each member's own pages.  One launch, no prompt pass.
-  const int tiles = rlda::kPackTiles;
-  const int pack = std::min(std::min(rlda::kPackMaxMembers, rlda::kMaxGroup * tiles / h->group), group_size);
+  // Packed: up to 16 / G members of a group share the rows of one MFMA tile, so
+  // one segment streams the prompt pages once for all of them and then each
+  // member's own pages.  One launch, no prompt pass.
+  const int tiles = 1;
+  const int pack = std::min(std::min(rlda::kPackMaxMembers, rlda::kMaxGroup / h->group), group_size);
   const int ngroups = (batch + group_size - 1) / group_size, per_group = (group_size + pack - 1) / pack;
   // Packed runs read each prompt page once per pack, the prompt pass once per group
   // at a fixed cost (a second launch, its merge).  With the caller's prompt length
@@ -386,7 +386,7 @@ rlda_status rl_decode_attn_run_multi(rl_decode_attn_t h, int32_t batch, int32_t 
   // are held by a wave as one or two 16-row tiles against each page; more than 32
   // take two segments.  Otherwise the 128-row MFMA kernel.
   const int64_t rows = (int64_t)max_q_len * h->group;
-  int tiles = rows > rlda::kMaxGroup ? rlda::kMaxRowTiles : 1;
+  int tiles = rows > rlda::kMaxGroup && batch <= rlda::kTwoTileMaxBatch ? rlda::kMaxRowTiles : 1;
   int64_t row_chunks = (rows + rlda::kMaxGroup * tiles - 1) / (rlda::kMaxGroup * tiles);
   const bool rows_path = max_q_len >= 1 && max_q_len <= rlda::kMaxRowsQLen &&
                          rows <= (int64_t)rlda::kMaxGroup * rlda::kMaxRowChunks &&

@@ -121,9 +121,9 @@ __device__ __forceinline__ void store_row(const Params& p, int b, int qh, int d0
     for (int k = 0; k < N; k += 4) *(f32x4*)(dst + k) = f32x4{o[k] * inv, o[k + 1] * inv, o[k + 2] * inv, o[k + 3] * inv};
   }
 }
-template <int D>
+template <int D, int DPT = D / 16>
 __device__ __forceinline__ void store_out(const Params& p, int b, int qh, int d0, const float* o, float inv) {
-  store_row<D, D / 16>(p, b, qh, d0, o, inv);
+  store_row<D, DPT>(p, b, qh, d0, o, inv);
 }
 
 // Query heads of each KV head (a copy of Params::q_head, filled at kernel start):
@@ -162,11 +162,10 @@ __device__ __forceinline__ void lse_merge(float& M, float& Ls, float* o, float m
 // Merge the pieces of segment (b, g) held by workgroups u_first..u_last: the piece
 // of workgroup k is in slot 2k+1 when it continues past k's share, else in slot 2k.
 // Loads are issued kBatch pieces at a time (one round trip per batch), then merged
-// in piece order with a running maximum.  Thread (h, d0) merges its D/16 outputs.
-template <int D, int kBatch>
+// in piece order with a running maximum.  Thread (h, d0) merges its DPT outputs.
+template <int D, int kBatch, int DPT>
 __device__ __forceinline__ void merge_batches(const Params& p, const PartialRsrc& rs, int h, int d0, int64_t u_first,
                                               int64_t u_last, float& M, float& Ls, float* o) {
-  constexpr int DPT = D / 16;
   const int G = p.part_rows;
   for (int64_t k0 = u_first; k0 <= u_last; k0 += kBatch) {
     u32x2 ml[kBatch];
@@ -189,20 +188,20 @@ __device__ __forceinline__ void merge_batches(const Params& p, const PartialRsrc
 }
 
 // A segment cut into many pieces (a long sequence over few workgroups' worth of
-// other work) is merged 16 pieces per round trip; the common 2-4 pieces, 4 at a time.
-template <int D>
+// other work) is merged 16 pieces per round trip (8 when a thread holds 16 outputs);
+// the common 2-4 pieces, 4 at a time.
+template <int D, int DPT = D / 16>
 __device__ __forceinline__ void merge_pieces(const Params& p, int orow, int qh, int h, int d0, int64_t u_first,
                                              int64_t u_last) {
-  constexpr int DPT = D / 16;
   const PartialRsrc rs = PartialRsrc::of<D>(p);
   float M = neg_inf(), Ls = 0.f, o[DPT];
 #pragma unroll
   for (int e = 0; e < DPT; ++e) o[e] = 0.f;
   if (u_last - u_first >= 4)
-    merge_batches<D, 16>(p, rs, h, d0, u_first, u_last, M, Ls, o);
+    merge_batches<D, (DPT <= 8 ? 16 : 8), DPT>(p, rs, h, d0, u_first, u_last, M, Ls, o);
   else
-    merge_batches<D, 4>(p, rs, h, d0, u_first, u_last, M, Ls, o);
-  store_out<D>(p, orow, qh, d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
+    merge_batches<D, 4, DPT>(p, rs, h, d0, u_first, u_last, M, Ls, o);
+  store_out<D, DPT>(p, orow, qh, d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
 }
 
 // ---------------------------------------------------------------- MFMA policy
@@ -741,9 +740,13 @@ __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgp
 void decode_attention_kernel(const Params p) {
   static_assert(NT == 1 || (MULTI && NT == 2), "two row tiles only for multi-token rows");
   static_assert(!PACK || MULTI, "packed grouped runs use the multi-token row machinery");
+  static_assert(!(PACK && NT == 2), "packed grouped runs hold one tile");
   constexpr int D = Pol::kD;
-  constexpr int DPT = D / 16;   // output elements per thread in the workgroup merge
-  constexpr int kB = PACK ? kPackMaxBatch : kMaxBatch;
+  // Workgroup merge: kMR rows per slot (both tiles of a two-tile segment), kTPR
+  // threads per row, DPT output elements per thread.
+  constexpr int kMR = 16 * NT, kTPR = kThreads / kMR;
+  constexpr int DPT = D / kTPR;
+  constexpr int kB = PACK ? kPackMaxBatch : (NT == 2 ? kTwoTileMaxBatch : kMaxBatch);
   // Units: sequences, or packs of group members (packed grouped runs).
   __shared__ int32_t s_pre[kB + 1];
   __shared__ uint8_t s_tail[kB];   // valid tokens of each sequence's last page
@@ -755,8 +758,8 @@ void decode_attention_kernel(const Params p) {
   __shared__ int16_t s_gpp[PACK ? kB : 1];
   // Cut pieces: slot 2w holds wave w's piece that began before its quarter of the
   // share, slot 2w+1 its piece that continues past it.
-  __shared__ __align__(16) float s_acc[2 * kWaves][16][D + 4];
-  __shared__ __align__(16) float s_ml[2 * kWaves][16][2];
+  __shared__ __align__(16) float s_acc[2 * kWaves][kMR][D + 4];
+  __shared__ __align__(16) float s_ml[2 * kWaves][kMR][2];
   __shared__ int32_t s_seg[2 * kWaves];
   __shared__ int32_t s_scan[kWaves];
   __shared__ int32_t s_last[2];
@@ -922,16 +925,13 @@ void decode_attention_kernel(const Params p) {
   //    written directly.
   const int64_t r0 = (int64_t)u * T / Wn, r1 = (int64_t)(u + 1) * T / Wn;
   const int w0 = (int)(r0 + (r1 - r0) * wave / kWaves), w1 = (int)(r0 + (r1 - r0) * (wave + 1) / kWaves);
-  // Two-tile segments: tile 1's running state, and tile 1 of the wave's first
-  // piece (slot 2w), both kept for the second pass of the workgroup merge.
-  Pol st2, held;
   // Q operands of the NT tiles, loaded with a segment's first page.
   struct QN {
     typename Pol::QOp t[NT];
   };
   if (w0 < w1) {
     constexpr int kDepth = Pol::kDepth;
-    Pol st;
+    Pol st, st2;   // st2: the second tile of a two-tile segment
     st.setup(p, lane, p.stride_slot);
     QN qring[kDepth];
     typename Pol::PInit pring[kDepth];
@@ -1051,9 +1051,7 @@ void decode_attention_kernel(const Params p) {
           } else {
             const int slot = 2 * wave + (ended ? 0 : 1);
             st.to_lds(s_acc[slot], s_ml[slot], lane);
-            if constexpr (NT == 2) {
-              if (ended) held = st2;   // slot 2w+1 is the quarter's last piece: st2 keeps it
-            }
+            if constexpr (NT == 2) st2.to_lds(s_acc[slot] + 16, s_ml[slot] + 16, lane);
             if (lane == 0) s_seg[slot] = b * Hs + (MULTI ? g * nrc + chunk_of_info(info) : g);
           }
         }
@@ -1089,31 +1087,20 @@ void decode_attention_kernel(const Params p) {
   //    are consecutive; together they are either the whole segment (normalise and
   //    write) or this workgroup's piece of a segment cut at the share boundary
   //    (published as a partial).
-  const int h = tid >> 4, d0 = (tid & 15) * DPT;
-  // Tile t of segment gv of sequence b: its rows, and the output row / query head
-  // of this thread's row h (multi-token runs: row 16 NT rc + 16 t + h of the
-  // (sequence, KV head)).
-  auto seg_row = [&](int gv, int t) { return kSegRows * (gv % nrc) + 16 * t + h; };
-  auto seg_rows = [&](int b, int gv, int t) {
-    return MULTI ? min(kPage, (s_ppre[b] & 31) * G - kSegRows * (gv % nrc) - 16 * t) : G;
+  const int h = tid / kTPR, d0 = (tid % kTPR) * DPT;
+  // Segment gv of sequence b: its rows, and the output row / query head of this
+  // thread's row h (multi-token runs: row 16 NT rc + h of the (sequence, KV head)).
+  auto seg_row = [&](int gv) { return kSegRows * (gv % nrc) + h; };
+  auto seg_rows = [&](int b, int gv) {
+    return MULTI ? min(kSegRows, (s_ppre[b] & 31) * G - kSegRows * (gv % nrc)) : G;
   };
-  auto out_row = [&](int b, int gv, int t) { return MULTI ? (s_ppre[b] >> 5) + seg_row(gv, t) / G : b; };
-  auto out_head = [&](int gv, int t) {
-    return MULTI ? s_qhead[(gv / nrc) * G + seg_row(gv, t) % G] : s_qhead[gv * G + h];
+  auto out_row = [&](int b, int gv) { return MULTI ? (s_ppre[b] >> 5) + seg_row(gv) / G : b; };
+  auto out_head = [&](int gv) {
+    return MULTI ? s_qhead[(gv / nrc) * G + seg_row(gv) % G] : s_qhead[gv * G + h];
   };
   int hand_seg[2] = {-1, -1};
   int nhand = 0;
-  // One pass per row tile; the second pass merges the tile-1 states of the same slots.
-#pragma unroll 1
-  for (int t = 0; t < NT; ++t) {
-    if constexpr (NT == 2) {
-      if (t > 0) {
-        __syncthreads();   // the first pass has read the slots
-        if (s_seg[2 * wave] != -1) held.to_lds(s_acc[2 * wave], s_ml[2 * wave], lane);
-        if (s_seg[2 * wave + 1] != -1) st2.to_lds(s_acc[2 * wave + 1], s_ml[2 * wave + 1], lane);
-        __syncthreads();
-      }
-    }
+  {
     int cur = -1;   // segment of the group being merged
     float M = neg_inf(), Ls = 0.f, o[DPT];
 #pragma unroll
@@ -1124,24 +1111,23 @@ void decode_attention_kernel(const Params p) {
       const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
       const int64_t seg_start = (int64_t)Hs * pre_b + (int64_t)g * nb, seg_end = seg_start + nb;
       const bool whole = seg_start >= r0 && seg_end <= r1;
-      if (h < seg_rows(b, g, t)) {
+      if (h < seg_rows(b, g)) {
         if (whole) {
-          store_out<D>(p, out_row(b, g, t), out_head(g, t), d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
+          store_out<D, DPT>(p, out_row(b, g), out_head(g), d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
         } else {
           const PartialRsrc rs = PartialRsrc::of<D>(p);
           const int gs = (seg_end > r1) ? 2 * u + 1 : 2 * u;
-          const int R = p.part_rows, hr = 16 * t + h;   // the row within the slot
+          const int R = p.part_rows, hr = h;   // the row within the slot
 #pragma unroll
           for (int c = 0; c < DPT; c += 4)
             __builtin_amdgcn_raw_buffer_store_b128(*(const u32x4*)&o[c], rs.acc, ((gs * R + hr) * D + d0 + c) * 4, 0,
                                                    kDeviceScope);
-          if ((tid & 15) == 0)
+          if (tid % kTPR == 0)   // one thread per row stores its (m, l)
             __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(M), __float_as_uint(Ls)}, rs.ml,
                                                   (gs * R + hr) * 8, 0, kDeviceScope);
         }
       }
-      // Only the first and last group can be cut; the second pass sees the same groups.
-      if (t == 0 && !whole && nhand < 2) hand_seg[nhand++] = cur;
+      if (!whole && nhand < 2) hand_seg[nhand++] = cur;   // only the first and last group can be cut
     };
     // Slots in position order; the used slots of one segment are consecutive.  Each
     // step issues its LDS reads (tag, max/sum, partial output) together.
@@ -1166,7 +1152,7 @@ void decode_attention_kernel(const Params p) {
 #pragma unroll
         for (int e = 0; e < DPT; ++e) o[e] = 0.f;
       }
-      if (sj >= 0 && h < seg_rows(sj / Hs, sj - (sj / Hs) * Hs, t)) lse_merge<DPT>(M, Ls, o, mj, lj, v);
+      if (sj >= 0 && h < seg_rows(sj / Hs, sj - (sj / Hs) * Hs)) lse_merge<DPT>(M, Ls, o, mj, lj, v);
     }
   }
 
@@ -1190,11 +1176,9 @@ void decode_attention_kernel(const Params p) {
     const int b = sgi / Hs, g = sgi - b * Hs;
     const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
     const int64_t seg_start = (int64_t)Hs * pre_b + (int64_t)g * nb;
-#pragma unroll 1
-    for (int t = 0; t < NT; ++t)
-      if (h < seg_rows(b, g, t))
-        merge_pieces<D>(p, out_row(b, g, t), out_head(g, t), 16 * t + h, d0, owner_of(seg_start, Wn, T),
-                        owner_of(seg_start + nb - 1, Wn, T));
+    if (h < seg_rows(b, g))
+      merge_pieces<D, DPT>(p, out_row(b, g), out_head(g), h, d0, owner_of(seg_start, Wn, T),
+                           owner_of(seg_start + nb - 1, Wn, T));
     if (tid == 0) atomicExch(p.counters + sgi, 0u);
   }
 }
@@ -1534,8 +1518,7 @@ int launch_rows(int tiles, const Params& p, void* stream, void* ev_begin, void* 
 
 template <class Pol>
 int launch_packed(int tiles, const Params& p, void* stream, void* ev_begin, void* ev_end) {
-  return tiles == 2 ? launch<Pol, true, 2, true>(p, stream, ev_begin, ev_end)
-                    : launch<Pol, true, 1, true>(p, stream, ev_begin, ev_end);
+  return tiles == 1 ? launch<Pol, true, 1, true>(p, stream, ev_begin, ev_end) : -1;
 }
 
 int launch_decode_rows(KvKind kind, int head_dim, int tiles, const Params& p, void* stream, void* ev_begin,

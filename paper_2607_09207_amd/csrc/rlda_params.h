@@ -105,9 +105,7 @@ constexpr int kMultiMaxBatch = 4096;   // its per-sequence LDS table stays withi
 constexpr int kPackMaxBatch = 4096;    // packed grouped runs: per-sequence and per-pack LDS tables of this size
 constexpr int kPackMaxMembers = 7;     // ... members per pack (3 bits of the page descriptor, 7 = every member)
 constexpr int kPackMaxPages = 32767;   // ... pages per sequence (16-bit LDS entries)
-#ifndef RLDA_PACK_TILES
-#define RLDA_PACK_TILES 1          // 16-row tiles a wave holds per pack (1 or 2)
-#endif
-constexpr int kPackTiles = RLDA_PACK_TILES;
+constexpr int kTwoTileMaxBatch = 2048;   // two-tile multi-token rows: per-sequence LDS tables of this size
+                                         // leave room for 32-row merge slots
 
 }  // namespace rlda

@@ -147,3 +147,16 @@ def test_rows_path_two_tiles_many_short_sequences(torch_cuda, ranges):
     got, flags = run_multi(torch_cuda, w, handle=h, tag=f"rows two tiles ranges={ranges}", max_q_len=4)
     assert flags == 0
     assert_close(got, oracle.run_multi(w), "bf16", f"rows path two tiles ranges={ranges}")
+
+
+@pytest.mark.parametrize("batch", [2048, 2049])
+def test_two_tile_batch_limit(torch_cuda, batch):
+    # 28 rows per (sequence, KV head): two tiles up to 2048 sequences, beyond that two
+    # one-tile segments; the values are the operation's either way.
+    rng = np.random.default_rng(87)
+    lens = rng.integers(4, 60, size=batch)
+    w = I.make_multi(lens.tolist(), [4] * batch, 28, 4, 128, q_dtype="bf16", kv_dtype="bf16", seed=88,
+                     max_pages_per_seq=4)
+    got, flags = run_multi(torch_cuda, w, tag=f"two-tile limit B={batch}", max_q_len=4)
+    assert flags == 0
+    assert_close(got, oracle.run_multi(w), "bf16", f"rows path B={batch}")
