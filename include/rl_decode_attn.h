@@ -235,8 +235,10 @@ rlda_status rl_decode_attn_append(rl_decode_attn_t handle, int32_t batch, int32_
  *                1 <= max_q_len <= 16 and max_q_len * G <= 64 (and batch * Hkv *
  *                max_pages_per_seq * ceil(max_q_len * G / 16) < 2^31), the call runs
  *                on the decode kernel's page stream (the n_b * G rows of each
- *                (sequence, KV head) as up to four 16-row MFMA tiles, each streaming
- *                the pages, long sequences split across workgroups; workspace as
+ *                (sequence, KV head) as 16-row MFMA tiles, one wave holding two of
+ *                them against each page when batch <= 2048, up to four segments
+ *                that each stream the pages, long sequences split across
+ *                workgroups; workspace as
  *                for rl_decode_attn_run, counters included); a sequence with
  *                n_b > max_q_len then gets no rows and raises flag bit 1.  Otherwise
  *                the (token, head) pairs of one (sequence, KV head) are processed 128
