@@ -102,9 +102,9 @@ __device__ __forceinline__ float group_sum(float x) {
 
 // ---------------------------------------------------------------- helpers
 
-__device__ __forceinline__ int64_t owner_of(int64_t x, int W, int64_t T) {
-  // Largest u with floor(u*T/W) <= x.
-  return ((x + 1) * (int64_t)W - 1) / T;
+__device__ __forceinline__ int64_t owner_of(int64_t x, int W, int64_t C) {
+  // Largest u with floor(u*C/W) <= x: the share holding cost x.
+  return ((x + 1) * (int64_t)W - 1) / C;
 }
 
 // Write N consecutive output elements o[0..N) * inv of row (b, qh) starting at d0.
@@ -760,8 +760,10 @@ void decode_attention_kernel(const Params p) {
   // share, slot 2w+1 its piece that continues past it.
   __shared__ __align__(16) float s_acc[2 * kWaves][kMR][D + 4];
   __shared__ __align__(16) float s_ml[2 * kWaves][kMR][2];
+  // Non-empty units before each unit (the work split prices every segment's start).
+  __shared__ uint16_t s_ne[kB + 1];
   __shared__ int32_t s_seg[2 * kWaves];
-  __shared__ int32_t s_scan[kWaves];
+  __shared__ int32_t s_scan[kWaves], s_scan_ne[kWaves];
   __shared__ int32_t s_last[2];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
@@ -817,7 +819,7 @@ void decode_attention_kernel(const Params p) {
   {
     const int per = (nunits + kThreads - 1) / kThreads;
     const int lo = min(tid * per, nunits), hi = min(lo + per, nunits);
-    int sum = 0, bad = 0;
+    int sum = 0, cnt = 0, bad = 0;   // pages, non-empty units
     for (int b = lo; b < hi; ++b) {
       if constexpr (PACK) {
         // Pack b: members b0 .. b0 + np - 1 of group i; the prompt once, then each member's own pages.
@@ -830,6 +832,7 @@ void decode_attention_kernel(const Params p) {
         s_ppre[b] = (b0 << 5) | np;
         s_pre[b + 1] = n;
         sum += n;
+        cnt += n > 0;
         continue;
       }
       int L = p.seq_lens[b];
@@ -859,28 +862,51 @@ void decode_attention_kernel(const Params p) {
       s_pre[b + 1] = n;
       s_tail[b] = (uint8_t)(L - (nfull - 1) * kPage);   // 1..16 when nfull > 0
       sum += n;
+      cnt += n > 0;
     }
     if (bad && u == 0) atomicOr(p.flags, kFlagBadLen);
-    int x = sum;
+    int x = sum, xn = cnt;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(x, o);
-      if (lane >= o) x += y;
+      const int y = __shfl_up(x, o), yn = __shfl_up(xn, o);
+      if (lane >= o) {
+        x += y;
+        xn += yn;
+      }
     }
-    if (lane == 63) s_scan[wave] = x;
+    if (lane == 63) {
+      s_scan[wave] = x;
+      s_scan_ne[wave] = xn;
+    }
     for (int e = tid; e < p.num_q_heads; e += kThreads) s_qhead[e] = p.q_head[e];
     if (tid < 2 * kWaves) s_seg[tid] = -1;
     __syncthreads();
-    int run = x - sum;
-    for (int w = 0; w < wave; ++w) run += s_scan[w];
+    int run = x - sum, rne = xn - cnt;
+    for (int w = 0; w < wave; ++w) {
+      run += s_scan[w];
+      rne += s_scan_ne[w];
+    }
     for (int b = lo; b < hi; ++b) {
-      run += s_pre[b + 1];
+      const int n = s_pre[b + 1];
+      s_ne[b] = (uint16_t)rne;
+      rne += n > 0;
+      run += n;
       s_pre[b + 1] = run;
     }
-    if (tid == 0) s_pre[0] = 0;
+    if (tid == kThreads - 1) s_ne[nunits] = (uint16_t)rne;   // the last thread's range ends at nunits
+    if (tid == 0) {
+      s_pre[0] = 0;
+      s_ne[0] = 0;
+    }
     __syncthreads();
   }
   const int64_t T = uni64((int64_t)s_pre[nunits] * Hs);
+  // Cost of the flattened list: one per position, and one more per segment of a
+  // non-empty unit for its start (loading Q, opening and closing the state cost
+  // about a page's time on the stream).  Unit b's segments begin at cost
+  // Hs (s_pre[b] + s_ne[b]), each nb + 1 long: its start, then its pages.
+  const int64_t C = uni64((int64_t)Hs * (s_pre[nunits] + s_ne[nunits]));
+  auto cost_of = [&](int64_t pos, int b, int gv) { return pos + (int64_t)Hs * s_ne[b] + gv + 1; };
 
   // 2. Sequences with no pages left to stream: zero rows, or (grouped runs) the
   //    normalised prompt-pass result when the prompt is the whole sequence.
@@ -915,16 +941,46 @@ void decode_attention_kernel(const Params p) {
     }
   }
 
-  // Never more shares than units: every share below Wn is non-empty.
+  // Never more shares than positions (C >= T >= Wn).  A share can still hold no
+  // position when the shares are shorter than two costs.
   const int Wn = (int)min((int64_t)W, T);
   if (u >= Wn) return;
 
   // 3. This workgroup's share [r0, r1) of the flattened (sequence, KV head, page)
-  //    list, and this wave's quarter [w0, w1) of it.  Each wave walks its own
-  //    pieces without waiting for the others; a piece inside its quarter is
-  //    written directly.
-  const int64_t r0 = (int64_t)u * T / Wn, r1 = (int64_t)(u + 1) * T / Wn;
-  const int w0 = (int)(r0 + (r1 - r0) * wave / kWaves), w1 = (int)(r0 + (r1 - r0) * (wave + 1) / kWaves);
+  //    list, and this wave's quarter [w0, w1) of it: equal parts of the cost
+  //    [floor(u C / Wn), floor((u + 1) C / Wn)), each taken as the positions whose
+  //    cost falls inside it.  Each wave walks its own pieces without waiting for
+  //    the others; a piece inside its quarter is written directly.
+  int w0, w1;
+  int64_t r0, r1;
+  {
+    // Lane i < 5 turns quarter boundary i into the first position of cost at least
+    // that boundary: the unit holding it (K(b) = Hs (s_pre[b] + s_ne[b]) <= B <
+    // K(b + 1)), then the segment and the page within it (the segment's start cost
+    // maps to its first page).
+    int rb = 0;
+    if (lane <= kWaves) {
+      const int64_t B0 = (int64_t)u * C / Wn, B1 = (int64_t)(u + 1) * C / Wn;
+      const int64_t B = B0 + (B1 - B0) * lane / kWaves;
+      if (B >= C) {
+        rb = (int)T;
+      } else {
+        int lo = 0, hi = nunits;
+        while (hi - lo > 1) {
+          const int mid = (lo + hi) >> 1;
+          if ((int64_t)Hs * (s_pre[mid] + s_ne[mid]) <= B) lo = mid; else hi = mid;
+        }
+        const int pre = s_pre[lo], nb = s_pre[lo + 1] - pre;
+        const int rem = (int)(B - (int64_t)Hs * (pre + s_ne[lo]));
+        const int gv = rem / (nb + 1), q = rem - gv * (nb + 1);
+        rb = Hs * pre + gv * nb + max(q - 1, 0);
+      }
+    }
+    r0 = __builtin_amdgcn_readfirstlane(rb);
+    r1 = __builtin_amdgcn_readlane(rb, kWaves);
+    w0 = __builtin_amdgcn_readlane(rb, wave);
+    w1 = __builtin_amdgcn_readlane(rb, wave + 1);
+  }
   // Q operands of the NT tiles, loaded with a segment's first page.
   struct QN {
     typename Pol::QOp t[NT];
@@ -1166,7 +1222,8 @@ void decode_attention_kernel(const Params p) {
     const int b = sgi / Hs, g = sgi - b * Hs;
     const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
     const int64_t seg_start = (int64_t)Hs * pre_b + (int64_t)g * nb;
-    const uint32_t npieces = (uint32_t)(owner_of(seg_start + nb - 1, Wn, T) - owner_of(seg_start, Wn, T) + 1);
+    const uint32_t npieces = (uint32_t)(owner_of(cost_of(seg_start + nb - 1, b, g), Wn, C) -
+                                        owner_of(cost_of(seg_start, b, g), Wn, C) + 1);
     s_last[tid] = (atomicAdd(p.counters + sgi, 1u) + 1u == npieces);
   }
   __syncthreads();
@@ -1177,8 +1234,8 @@ void decode_attention_kernel(const Params p) {
     const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
     const int64_t seg_start = (int64_t)Hs * pre_b + (int64_t)g * nb;
     if (h < seg_rows(b, g))
-      merge_pieces<D, DPT>(p, out_row(b, g), out_head(g), h, d0, owner_of(seg_start, Wn, T),
-                           owner_of(seg_start + nb - 1, Wn, T));
+      merge_pieces<D, DPT>(p, out_row(b, g), out_head(g), h, d0, owner_of(cost_of(seg_start, b, g), Wn, C),
+                           owner_of(cost_of(seg_start + nb - 1, b, g), Wn, C));
     if (tid == 0) atomicExch(p.counters + sgi, 0u);
   }
 }

@@ -1,62 +1,116 @@
 """Work-split arithmetic of the attention kernel, checked on the CPU.
 
-The kernel flattens (sequence, KV head, page) units in b-major, g-minor order and
-gives workgroup u the share [floor(u T / W), floor((u+1) T / W)) with W = min(ranges, T).
-A segment cut across shares is written as pieces: the piece of workgroup k goes to
-slot 2k+1 when it continues past k's share, else to slot 2k; owner(x) =
-floor(((x+1) W - 1) / T).  This test enumerates the shares directly and checks that
-the closed forms agree with them, that slots stay below 2W, that no two pieces of
-any segment share a slot, and that every split segment's piece count matches.
+The kernel flattens (sequence, KV head, page) positions in b-major, g-minor order
+(T of them) and prices them: every position costs one, and every segment (a
+non-empty sequence's KV head) one more for its start, so position p, page j of
+segment g of sequence b, has cost c(p) = p + Hs ne(b) + g + 1 (ne(b): non-empty
+sequences before b) out of C = T + Hs ne(batch).  Workgroup u takes the positions
+whose cost lies in [floor(u C / W), floor((u+1) C / W)) with W = min(ranges, T),
+and its waves the four equal cost parts of that.  A segment cut across shares is
+written as pieces: the piece of workgroup k goes to slot 2k+1 when it continues past
+k's share, else to slot 2k; owner(x) = floor(((x+1) W - 1) / C) is the share
+holding cost x.  These tests price every position one by one and check that the
+kernel's closed forms (the boundary search, the owner, the piece count) agree with
+that enumeration, that slots stay below 2W, that no two pieces share a slot, and
+that every share holds an equal cost.
 """
 import numpy as np
 import pytest
 
 
-def owner(x, W, T):
-    return ((x + 1) * W - 1) // T
+def owner(x, W, C):
+    return ((x + 1) * W - 1) // C
 
 
-def enumerate_pieces(lens, Hkv, ranges, P=16):
+def layout(lens, Hs, P=16):
     n = [(max(L, 0) + P - 1) // P for L in lens]
     pre = np.concatenate([[0], np.cumsum(n)]).astype(np.int64)
-    T = int(pre[-1]) * Hkv
+    ne = np.concatenate([[0], np.cumsum([x > 0 for x in n])]).astype(np.int64)
+    T = int(pre[-1]) * Hs
+    C = Hs * int(pre[-1] + ne[-1])
+    return pre, ne, T, C
+
+
+def position_of_cost(B, pre, ne, Hs, T, C):
+    """The kernel's boundary search: the first position whose cost is at least B."""
+    if B >= C:
+        return T
+    lo, hi = 0, len(pre) - 1
+    while hi - lo > 1:
+        mid = (lo + hi) >> 1
+        if Hs * (pre[mid] + ne[mid]) <= B:
+            lo = mid
+        else:
+            hi = mid
+    nb = int(pre[lo + 1] - pre[lo])
+    rem = int(B - Hs * (pre[lo] + ne[lo]))
+    gv, q = divmod(rem, nb + 1)
+    return int(Hs * pre[lo] + gv * nb + max(q - 1, 0))
+
+
+def enumerate_pieces(lens, Hs, ranges, P=16):
+    pre, ne, T, C = layout(lens, Hs, P)
     if T == 0:
-        return [], 0, 0
+        return [], 0, 0, 0, None
     W = min(ranges, T)
+    # every position priced one by one
+    cost = np.empty(T, np.int64)
+    seg_of = []
+    p = 0
+    for b in range(len(lens)):
+        nb = int(pre[b + 1] - pre[b])
+        for g in range(Hs if nb else 0):
+            for j in range(nb):
+                cost[p] = p + Hs * ne[b] + g + 1
+                seg_of.append((b, g, j, nb))
+                p += 1
+    assert p == T and np.all(np.diff(cost) > 0) and cost[-1] < C
+    bounds = [u * C // W for u in range(W + 1)]
+    share = np.searchsorted(np.array(bounds), cost, side="right") - 1
     pieces = []
-    for u in range(W):
-        r0, r1 = u * T // W, (u + 1) * T // W
-        assert r1 > r0
-        x = r0
-        while x < r1:
-            y = x // Hkv
-            b = int(np.searchsorted(pre, y, side="right") - 1)
-            nb = int(pre[b + 1] - pre[b])
-            off = x - Hkv * int(pre[b])
-            g, j0 = off // nb, off % nb
-            seg_start = x - j0
-            seg_end = seg_start + nb
-            pe = min(r1, seg_end)
-            whole = j0 == 0 and pe == seg_end
-            after = pe == r1 and pe < seg_end
-            slot = 2 * u + 1 if after else 2 * u
-            pieces.append(dict(u=u, b=b, g=g, j0=j0, j1=j0 + pe - x, whole=whole, slot=slot,
-                               seg=(seg_start, seg_end)))
-            x = pe
-    return pieces, T, W
+    x = 0
+    while x < T:
+        u = int(share[x])
+        b, g, j0, nb = seg_of[x]
+        seg_start = x - j0
+        seg_end = seg_start + nb
+        pe = x
+        while pe < seg_end and share[pe] == u:
+            pe += 1
+        r1 = int(np.searchsorted(share, u, side="right"))
+        whole = j0 == 0 and pe == seg_end
+        after = pe == r1 and pe < seg_end
+        slot = 2 * u + 1 if after else 2 * u
+        pieces.append(dict(u=u, b=b, g=g, j0=j0, j1=j0 + pe - x, whole=whole, slot=slot,
+                           seg=(seg_start, seg_end), cost=(int(cost[seg_start]), int(cost[seg_end - 1]))))
+        x = pe
+    return pieces, T, C, W, (share, bounds, pre, ne)
 
 
-@pytest.mark.parametrize("seed", range(12))
+@pytest.mark.parametrize("seed", range(16))
 def test_share_arithmetic_matches_enumeration(seed):
     rng = np.random.default_rng(seed)
     B = int(rng.integers(1, 40))
     lens = rng.integers(0, 3000, size=B)
     lens[rng.random(B) < 0.2] = 0
-    Hkv = int(rng.choice([1, 2, 4, 8]))
+    if seed % 4 == 3:   # many short sequences: segment starts dominate the cost
+        lens = rng.integers(0, 40, size=B)
+    Hs = int(rng.choice([1, 2, 3, 4, 8, 16]))
     ranges = int(rng.choice([1, 3, 7, 61, 512, 5000]))
-    pieces, T, W = enumerate_pieces(lens.tolist(), Hkv, ranges)
+    pieces, T, C, W, aux = enumerate_pieces(lens.tolist(), Hs, ranges)
     if T == 0:
         return
+    share, bounds, pre, ne = aux
+    # the closed-form boundary search gives each share's and each quarter's first position
+    for u in range(W):
+        B0, B1 = bounds[u], bounds[u + 1]
+        r0 = position_of_cost(B0, pre, ne, Hs, T, C)
+        r1 = position_of_cost(B1, pre, ne, Hs, T, C)
+        assert np.all(share[r0:r1] == u)
+        assert r0 == 0 or share[r0 - 1] < u
+        assert r1 == T or share[r1] > u
+        qs = [position_of_cost(B0 + (B1 - B0) * w // 4, pre, ne, Hs, T, C) for w in range(5)]
+        assert qs[0] == r0 and qs[4] == r1 and qs == sorted(qs)
     covered = {}
     by_seg = {}
     for pc in pieces:
@@ -66,11 +120,11 @@ def test_share_arithmetic_matches_enumeration(seed):
         for j in range(pc["j0"], pc["j1"]):
             assert (key, j) not in covered
             covered[(key, j)] = pc["u"]
-    # every unit covered exactly once
+    # every position covered exactly once
     assert len(covered) == T
     for key, ps in by_seg.items():
-        s0, s1 = ps[0]["seg"]
-        uf, ul = owner(s0, W, T), owner(s1 - 1, W, T)
+        c0, c1 = ps[0]["cost"]
+        uf, ul = owner(c0, W, C), owner(c1, W, C)
         assert [p["u"] for p in ps] == list(range(uf, ul + 1))
         if len(ps) == 1:
             assert ps[0]["whole"]
@@ -84,12 +138,28 @@ def test_share_arithmetic_matches_enumeration(seed):
     assert len(set(all_slots)) == len(all_slots)
 
 
-def test_each_share_holds_equal_work():
-    pieces, T, W = enumerate_pieces([20000, 16, 300, 5000], 8, 512)
+def test_each_share_holds_equal_cost():
+    """Pages plus segment starts per share differ by at most two (a start's cost can
+    fall just before the share that holds the segment's first page)."""
+    lens = [20000, 16, 300, 5000] + [17] * 40 + [3000]
+    pieces, T, C, W, _ = enumerate_pieces(lens, 8, 512)
     per = np.zeros(W, np.int64)
     for p in pieces:
-        per[p["u"]] += p["j1"] - p["j0"]
-    assert per.max() - per.min() <= 1
+        per[p["u"]] += p["j1"] - p["j0"] + (p["j0"] == 0)
+    assert per.max() - per.min() <= 2
+    assert abs(per.sum() - C) == 0
+
+
+def test_empty_shares_only_when_shares_are_shorter_than_two_costs():
+    for lens, Hs, ranges in [([16] * 50, 4, 200), ([16, 0, 0, 16], 2, 64), ([1] * 7, 1, 7)]:
+        pieces, T, C, W, aux = enumerate_pieces(lens, Hs, ranges)
+        share = aux[0]
+        empty = set(range(W)) - set(share.tolist())
+        if C // W >= 2:
+            assert not empty
+        # an empty share never owns a piece, and every owner between a segment's first
+        # and last holds one of its pieces
+        assert empty.isdisjoint({p["u"] for p in pieces})
 
 
 @pytest.mark.parametrize("W", list(range(1, 70)) + [255, 256, 257, 1024, 4095, 4096])
