@@ -76,7 +76,7 @@ typedef struct {
   int32_t page_size;              /* P: 16 */
   int32_t max_batch;              /* largest batch passed to run, 1..8192 */
   int32_t max_pages_per_seq;      /* block_table row length (elements); max_batch *
-                                     (max_pages_per_seq + 1) * num_kv_heads <= 2^31 - 1,
+                                     (max_pages_per_seq + 2) * num_kv_heads <= 2^31 - 1,
                                      else RLDA_ERR_UNSUPPORTED                       */
   rlda_dtype q_dtype, kv_dtype, out_dtype;
   const int32_t* kv_head_of_q;    /* HOST array [Hq] copied at create; NULL = h / G.
@@ -233,7 +233,7 @@ rlda_status rl_decode_attn_append(rl_decode_attn_t handle, int32_t batch, int32_
  *   total_q      host value: rows of q and out
  *   max_q_len    host value, 0 or an upper bound on every n_b.  When
  *                1 <= max_q_len <= 16 and max_q_len * G <= 64 (and batch * Hkv *
- *                (max_pages_per_seq + 1) * ceil(max_q_len * G / 16) < 2^31), the call runs
+ *                (max_pages_per_seq + 2) * ceil(max_q_len * G / 16) < 2^31), the call runs
  *                on the decode kernel's page stream (the n_b * G rows of each
  *                (sequence, KV head) as 16-row MFMA tiles, one wave holding two of
  *                them against each page when batch <= 2048, up to four segments

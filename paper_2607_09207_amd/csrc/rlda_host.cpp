@@ -96,8 +96,9 @@ rlda_status rl_decode_attn_create(const rl_decode_attn_config* cfg, rl_decode_at
   if (c.page_size != rlda::kPage) return RLDA_ERR_UNSUPPORTED;
   if (c.head_dim != 64 && c.head_dim != 128) return RLDA_ERR_UNSUPPORTED;
   // The kernel numbers (sequence, KV head, page) units, and prices their work with
-  // one more per (sequence, KV head), in 32-bit integers.
-  if ((int64_t)c.max_batch * (c.max_pages_per_seq + 1) * c.num_kv_heads > INT32_MAX) return RLDA_ERR_UNSUPPORTED;
+  // kStartCost more per (sequence, KV head), in 32-bit integers.
+  if ((int64_t)c.max_batch * (c.max_pages_per_seq + rlda::kStartCost) * c.num_kv_heads > INT32_MAX)
+    return RLDA_ERR_UNSUPPORTED;
   const int G = c.num_q_heads / c.num_kv_heads;
 
   rlda::KvKind kind;
@@ -391,7 +392,7 @@ rlda_status rl_decode_attn_run_multi(rl_decode_attn_t h, int32_t batch, int32_t 
   int64_t row_chunks = (rows + rlda::kMaxGroup * tiles - 1) / (rlda::kMaxGroup * tiles);
   const bool rows_path = max_q_len >= 1 && max_q_len <= rlda::kMaxRowsQLen &&
                          rows <= (int64_t)rlda::kMaxGroup * rlda::kMaxRowChunks &&
-                         (int64_t)batch * (c.max_pages_per_seq + 1) * c.num_kv_heads * row_chunks <= INT32_MAX;
+                         (int64_t)batch * (c.max_pages_per_seq + rlda::kStartCost) * c.num_kv_heads * row_chunks <= INT32_MAX;
   if (!rows_path && batch > rlda::kMultiMaxBatch) return RLDA_ERR_UNSUPPORTED;
   // The kernels address q with 32-bit byte offsets.
   if ((int64_t)total_q * c.num_q_heads * c.head_dim * 2 > INT32_MAX) return RLDA_ERR_UNSUPPORTED;

@@ -901,12 +901,13 @@ void decode_attention_kernel(const Params p) {
     __syncthreads();
   }
   const int64_t T = uni64((int64_t)s_pre[nunits] * Hs);
-  // Cost of the flattened list: one per position, and one more per segment of a
-  // non-empty unit for its start (loading Q, opening and closing the state cost
-  // about a page's time on the stream).  Unit b's segments begin at cost
-  // Hs (s_pre[b] + s_ne[b]), each nb + 1 long: its start, then its pages.
-  const int64_t C = uni64((int64_t)Hs * (s_pre[nunits] + s_ne[nunits]));
-  auto cost_of = [&](int64_t pos, int b, int gv) { return pos + (int64_t)Hs * s_ne[b] + gv + 1; };
+  // Cost of the flattened list: one per position, and kStartCost more per segment
+  // of a non-empty unit for its start (loading Q, opening and closing the state
+  // cost about a page's time on the stream).  Unit b's segments begin at cost
+  // K(b) = Hs (s_pre[b] + S s_ne[b]), each nb + S long: its start, then its pages.
+  constexpr int S = kStartCost;
+  const int64_t C = uni64((int64_t)Hs * (s_pre[nunits] + S * s_ne[nunits]));
+  auto cost_of = [&](int64_t pos, int b, int gv) { return pos + (int64_t)S * (Hs * s_ne[b] + gv + 1); };
 
   // 2. Sequences with no pages left to stream: zero rows, or (grouped runs) the
   //    normalised prompt-pass result when the prompt is the whole sequence.
@@ -955,9 +956,8 @@ void decode_attention_kernel(const Params p) {
   int64_t r0, r1;
   {
     // Lane i < 5 turns quarter boundary i into the first position of cost at least
-    // that boundary: the unit holding it (K(b) = Hs (s_pre[b] + s_ne[b]) <= B <
-    // K(b + 1)), then the segment and the page within it (the segment's start cost
-    // maps to its first page).
+    // that boundary: the unit holding it (K(b) <= B < K(b + 1)), then the segment
+    // and the page within it (the segment's start cost maps to its first page).
     int rb = 0;
     if (lane <= kWaves) {
       const int64_t B0 = (int64_t)u * C / Wn, B1 = (int64_t)(u + 1) * C / Wn;
@@ -968,12 +968,12 @@ void decode_attention_kernel(const Params p) {
         int lo = 0, hi = nunits;
         while (hi - lo > 1) {
           const int mid = (lo + hi) >> 1;
-          if ((int64_t)Hs * (s_pre[mid] + s_ne[mid]) <= B) lo = mid; else hi = mid;
+          if ((int64_t)Hs * (s_pre[mid] + S * s_ne[mid]) <= B) lo = mid; else hi = mid;
         }
         const int pre = s_pre[lo], nb = s_pre[lo + 1] - pre;
-        const int rem = (int)(B - (int64_t)Hs * (pre + s_ne[lo]));
-        const int gv = rem / (nb + 1), q = rem - gv * (nb + 1);
-        rb = Hs * pre + gv * nb + max(q - 1, 0);
+        const int rem = (int)(B - (int64_t)Hs * (pre + S * s_ne[lo]));
+        const int gv = rem / (nb + S), q = rem - gv * (nb + S);
+        rb = Hs * pre + gv * nb + max(q - S, 0);
       }
     }
     r0 = __builtin_amdgcn_readfirstlane(rb);

@@ -16,6 +16,10 @@ constexpr int kMaxRowChunks = 4;   // multi-token rows through the decode kernel
 #define RLDA_MAX_ROW_TILES 2       // 16-row tiles a wave holds against each page on that path (1 or 2)
 #endif
 constexpr int kMaxRowTiles = RLDA_MAX_ROW_TILES;
+#ifndef RLDA_START_COST
+#define RLDA_START_COST 2          // work-split cost of a segment's start, in pages
+#endif
+constexpr int kStartCost = RLDA_START_COST;
 constexpr int kMaxRowsQLen = 16;   // ... and at most 16 rows per sequence (a full page's token count, clamped
                                    // to 31, less a row's causal shift of up to 15 still covers the page)
 

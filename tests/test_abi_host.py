@@ -79,7 +79,7 @@ def test_create_accepts_the_workload_configurations(lib):
     (dict(softmax_scale=-1.0), -1),
     (dict(num_work_ranges=5000), -1),
     (dict(max_batch=8192, max_pages_per_seq=65536, num_kv_heads=4, num_q_heads=28), -2),   # > 2^31 units
-    # 8192 * 65535 * 4 units fit, but not with one more cost per (sequence, KV head)
+    # 8192 * 65535 * 4 units fit, but not with the start costs of the (sequence, KV head) segments
     (dict(max_batch=8192, max_pages_per_seq=65535, num_kv_heads=4, num_q_heads=28), -2),
 ])
 def test_create_rejects_bad_configurations(lib, kw, want):

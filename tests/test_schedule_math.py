@@ -2,9 +2,9 @@
 
 The kernel flattens (sequence, KV head, page) positions in b-major, g-minor order
 (T of them) and prices them: every position costs one, and every segment (a
-non-empty sequence's KV head) one more for its start, so position p, page j of
-segment g of sequence b, has cost c(p) = p + Hs ne(b) + g + 1 (ne(b): non-empty
-sequences before b) out of C = T + Hs ne(batch).  Workgroup u takes the positions
+non-empty sequence's KV head) S more for its start (the library's S is 2), so
+position p, page j of segment g of sequence b, has cost c(p) = p + S (Hs ne(b) +
+g + 1) (ne(b): non-empty sequences before b) out of C = T + S Hs ne(batch).  Workgroup u takes the positions
 whose cost lies in [floor(u C / W), floor((u+1) C / W)) with W = min(ranges, T),
 and its waves the four equal cost parts of that.  A segment cut across shares is
 written as pieces: the piece of workgroup k goes to slot 2k+1 when it continues past
@@ -22,34 +22,34 @@ def owner(x, W, C):
     return ((x + 1) * W - 1) // C
 
 
-def layout(lens, Hs, P=16):
+def layout(lens, Hs, P=16, S=1):
     n = [(max(L, 0) + P - 1) // P for L in lens]
     pre = np.concatenate([[0], np.cumsum(n)]).astype(np.int64)
     ne = np.concatenate([[0], np.cumsum([x > 0 for x in n])]).astype(np.int64)
     T = int(pre[-1]) * Hs
-    C = Hs * int(pre[-1] + ne[-1])
+    C = Hs * int(pre[-1] + S * ne[-1])
     return pre, ne, T, C
 
 
-def position_of_cost(B, pre, ne, Hs, T, C):
+def position_of_cost(B, pre, ne, Hs, T, C, S=1):
     """The kernel's boundary search: the first position whose cost is at least B."""
     if B >= C:
         return T
     lo, hi = 0, len(pre) - 1
     while hi - lo > 1:
         mid = (lo + hi) >> 1
-        if Hs * (pre[mid] + ne[mid]) <= B:
+        if Hs * (pre[mid] + S * ne[mid]) <= B:
             lo = mid
         else:
             hi = mid
     nb = int(pre[lo + 1] - pre[lo])
-    rem = int(B - Hs * (pre[lo] + ne[lo]))
-    gv, q = divmod(rem, nb + 1)
-    return int(Hs * pre[lo] + gv * nb + max(q - 1, 0))
+    rem = int(B - Hs * (pre[lo] + S * ne[lo]))
+    gv, q = divmod(rem, nb + S)
+    return int(Hs * pre[lo] + gv * nb + max(q - S, 0))
 
 
-def enumerate_pieces(lens, Hs, ranges, P=16):
-    pre, ne, T, C = layout(lens, Hs, P)
+def enumerate_pieces(lens, Hs, ranges, P=16, S=1):
+    pre, ne, T, C = layout(lens, Hs, P, S)
     if T == 0:
         return [], 0, 0, 0, None
     W = min(ranges, T)
@@ -61,7 +61,7 @@ def enumerate_pieces(lens, Hs, ranges, P=16):
         nb = int(pre[b + 1] - pre[b])
         for g in range(Hs if nb else 0):
             for j in range(nb):
-                cost[p] = p + Hs * ne[b] + g + 1
+                cost[p] = p + S * (Hs * ne[b] + g + 1)
                 seg_of.append((b, g, j, nb))
                 p += 1
     assert p == T and np.all(np.diff(cost) > 0) and cost[-1] < C
@@ -87,8 +87,9 @@ def enumerate_pieces(lens, Hs, ranges, P=16):
     return pieces, T, C, W, (share, bounds, pre, ne)
 
 
+@pytest.mark.parametrize("S", [1, 2, 3])
 @pytest.mark.parametrize("seed", range(16))
-def test_share_arithmetic_matches_enumeration(seed):
+def test_share_arithmetic_matches_enumeration(seed, S):
     rng = np.random.default_rng(seed)
     B = int(rng.integers(1, 40))
     lens = rng.integers(0, 3000, size=B)
@@ -97,19 +98,19 @@ def test_share_arithmetic_matches_enumeration(seed):
         lens = rng.integers(0, 40, size=B)
     Hs = int(rng.choice([1, 2, 3, 4, 8, 16]))
     ranges = int(rng.choice([1, 3, 7, 61, 512, 5000]))
-    pieces, T, C, W, aux = enumerate_pieces(lens.tolist(), Hs, ranges)
+    pieces, T, C, W, aux = enumerate_pieces(lens.tolist(), Hs, ranges, S=S)
     if T == 0:
         return
     share, bounds, pre, ne = aux
     # the closed-form boundary search gives each share's and each quarter's first position
     for u in range(W):
         B0, B1 = bounds[u], bounds[u + 1]
-        r0 = position_of_cost(B0, pre, ne, Hs, T, C)
-        r1 = position_of_cost(B1, pre, ne, Hs, T, C)
+        r0 = position_of_cost(B0, pre, ne, Hs, T, C, S)
+        r1 = position_of_cost(B1, pre, ne, Hs, T, C, S)
         assert np.all(share[r0:r1] == u)
         assert r0 == 0 or share[r0 - 1] < u
         assert r1 == T or share[r1] > u
-        qs = [position_of_cost(B0 + (B1 - B0) * w // 4, pre, ne, Hs, T, C) for w in range(5)]
+        qs = [position_of_cost(B0 + (B1 - B0) * w // 4, pre, ne, Hs, T, C, S) for w in range(5)]
         assert qs[0] == r0 and qs[4] == r1 and qs == sorted(qs)
     covered = {}
     by_seg = {}
@@ -139,15 +140,17 @@ def test_share_arithmetic_matches_enumeration(seed):
 
 
 def test_each_share_holds_equal_cost():
-    """Pages plus segment starts per share differ by at most two (a start's cost can
-    fall just before the share that holds the segment's first page)."""
+    """Pages plus priced segment starts per share differ by at most 2 S + 1: the cost
+    parts differ by one, and at each end of a share a start's S costs can fall before
+    the share that holds the segment's first page."""
     lens = [20000, 16, 300, 5000] + [17] * 40 + [3000]
-    pieces, T, C, W, _ = enumerate_pieces(lens, 8, 512)
-    per = np.zeros(W, np.int64)
-    for p in pieces:
-        per[p["u"]] += p["j1"] - p["j0"] + (p["j0"] == 0)
-    assert per.max() - per.min() <= 2
-    assert abs(per.sum() - C) == 0
+    for S in (1, 2):
+        pieces, T, C, W, _ = enumerate_pieces(lens, 8, 512, S=S)
+        per = np.zeros(W, np.int64)
+        for p in pieces:
+            per[p["u"]] += p["j1"] - p["j0"] + S * (p["j0"] == 0)
+        assert per.max() - per.min() <= 2 * S + 1
+        assert per.sum() == C
 
 
 def test_empty_shares_only_when_shares_are_shorter_than_two_costs():
