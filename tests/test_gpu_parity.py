@@ -108,6 +108,26 @@ def test_empty_sequences_give_zero_rows(torch_cuda):
         assert_close(got, oracle.run(w), "bf16", "empty")
 
 
+def test_shares_shorter_than_a_segment_start(torch_cuda):
+    """The work split prices a (sequence, KV head) start at two pages; with more work
+    ranges than that cost covers, some shares hold no page at all and every short
+    segment is cut or starts at a share edge.  Many empty sequences add no cost."""
+    rng = np.random.default_rng(21)
+    lens = rng.integers(0, 40, size=300)
+    lens[rng.random(300) < 0.3] = 0
+    lens[7] = 3000
+    w = I.make_custom(lens.tolist(), 8, 4, 128, q_dtype="bf16", kv_dtype="bf16", seed=21)
+    pages = int(sum((int(L) + 15) // 16 for L in lens))
+    T, C = 4 * pages, 4 * pages + 2 * 4 * int((lens > 0).sum())
+    for ranges in (4096, T // 2, 257):
+        if ranges == 4096:
+            assert C < 3 * T   # some shares cover only start costs
+        got, flags = gpu_run(torch_cuda, w, ranges=ranges, tag=f"fine shares ranges={ranges}")
+        assert flags == 0
+        assert np.all(got[lens == 0] == 0.0)
+        assert_close(got, oracle.run(w), "bf16", f"fine shares ranges={ranges}")
+
+
 def test_all_sequences_empty(torch_cuda):
     w = I.make_custom([0, 0, 0], 4, 4, 64, q_dtype="f32", kv_dtype="f32", seed=2, max_pages_per_seq=4)
     got, _ = gpu_run(torch_cuda, w, tag="all-empty")
