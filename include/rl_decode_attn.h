@@ -87,7 +87,7 @@ typedef struct {
   int64_t kv_stride_slot;         /* [page][kv_head][slot][d].  Must keep each row     */
                                   /* 16-byte aligned; slot stride >= head_dim.         */
   int32_t num_work_ranges;        /* 0 = fill the GPU (default).  > 0 forces how many
-                                     equal shares the KV work is cut into (tuning and
+                                     equal-cost shares the KV work is cut into (tuning and
                                      tests of the split/merge path); at most 4096.     */
 } rl_decode_attn_config;
 

@@ -5,11 +5,12 @@
 // App. A.1.2):
 //
 //   1. Work plan.  Every workgroup scans seq_lens into page-count prefix sums in
-//      LDS.  The work is the flattened list of (sequence, KV head, page) units;
-//      workgroup u owns the u-th of nranges equal shares of it.  Long sequences
-//      are therefore cut across many workgroups and short ones packed together:
-//      every workgroup streams the same number of KV pages however long the tail
-//      of the length distribution is (Sec. 2.3 on long-tail decode).
+//      LDS.  The work is the flattened list of (sequence, KV head, page) units,
+//      priced one per page plus a fixed start cost per (sequence, KV head);
+//      workgroup u owns the u-th of nranges equal-cost shares of it.  Long
+//      sequences are therefore cut across many workgroups and short ones packed
+//      together: every workgroup streams the same work however long the tail of
+//      the length distribution is (Sec. 2.3 on long-tail decode).
 //   2. Page gather.  Each of the 4 waves of a workgroup takes a quarter of the
 //      share and walks it as one continuous stream of pages: its lanes decode 64
 //      positions at a time (sequence, KV head, page id, valid tokens, segment

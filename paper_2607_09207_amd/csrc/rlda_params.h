@@ -51,7 +51,7 @@ struct Params {
   int32_t num_kv_heads;
   int32_t group;               // G = Hq / Hkv
   int32_t max_pages;           // block-table row length
-  int32_t nranges;             // workgroups = equal shares of the flattened work
+  int32_t nranges;             // workgroups = equal-cost shares of the flattened work
   float scale_log2;            // softmax scale * log2(e)
   int32_t out_bf16;            // 0: fp32 output, 1: bf16 output
   // Shared-prompt (grouped) runs; all null / 0 otherwise.
