@@ -66,22 +66,25 @@ struct RowLoad;
 template <>
 struct RowLoad<16> {
   typedef u32x4 type;
+  template <int CP = kLoadNT>
   static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
-    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kLoadNT);
+    return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, CP);
   }
 };
 template <>
 struct RowLoad<8> {
   typedef u32x2 type;
+  template <int CP = kLoadNT>
   static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
-    return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kLoadNT);
+    return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, CP);
   }
 };
 template <>
 struct RowLoad<4> {
   typedef uint32_t type;
+  template <int CP = kLoadNT>
   static __device__ __forceinline__ type load(__amdgpu_buffer_rsrc_t r, int off) {
-    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kLoadNT);
+    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, CP);
   }
 };
 
@@ -353,11 +356,12 @@ struct Mfma {
     q = qo;
   }
 
+  template <int CP = kLoadNT>
   __device__ __forceinline__ void issue(Frag& f, __amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv) const {
 #pragma unroll
-    for (int s = 0; s < KL; ++s) f.k[s] = RowLoad<16>::load(rk, koff[s]);
+    for (int s = 0; s < KL; ++s) f.k[s] = RowLoad<16>::template load<CP>(rk, koff[s]);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) f.v[r] = RowLoad<VB>::load(rv, voff[r]);
+    for (int r = 0; r < 4; ++r) f.v[r] = RowLoad<VB>::template load<CP>(rv, voff[r]);
   }
 
   __device__ __forceinline__ static bf16x8 k_operand(const Frag& f, int s) {
@@ -727,6 +731,11 @@ __device__ __forceinline__ StreamChunk fetch_chunk(const Params& p, const int32_
 
 // ---------------------------------------------------------------- the kernel
 
+#ifndef RLDA_PROMPT_TEMPORAL
+#define RLDA_PROMPT_TEMPORAL 1
+#endif
+constexpr bool kPromptTemporal = RLDA_PROMPT_TEMPORAL;
+
 // MULTI: multi-token rows (rl_decode_attn_run_multi with at most 16 NT row_chunks
 // rows per (sequence, KV head)): (b, g) has n_b * G rows, row r is query head
 // (r % G) of query row q_start[b] + r / G and sees keys below L - n_b + r / G + 1;
@@ -1029,7 +1038,18 @@ void decode_attention_kernel(const Params p) {
         const int64_t po = (pk >= 0) ? (int64_t)pk * p.stride_page + (int64_t)g * p.stride_head : 0;
         const int ptok = MULTI ? min(tok, kPage) : tok;   // tokens of this page
         const uint32_t nrec = ptok > 0 ? (uint32_t)((ptok - 1) * p.stride_slot + D * Pol::kEB) : 0u;
-        st.issue(f, make_rsrc_uni((const char*)p.k + po, nrec), make_rsrc_uni((const char*)p.v + po, nrec));
+        const __amdgpu_buffer_rsrc_t rk = make_rsrc_uni((const char*)p.k + po, nrec);
+        const __amdgpu_buffer_rsrc_t rv = make_rsrc_uni((const char*)p.v + po, nrec);
+        if constexpr (PACK && kPromptTemporal) {
+          // A group's prompt page is read by each of its packs, which run at about
+          // the same time on one XCD: keep it in the L2 for the other packs.
+          if (((info >> kInfoActShift) & 7) == kActAll)
+            st.template issue<0>(f, rk, rv);
+          else
+            st.issue(f, rk, rv);
+        } else {
+          st.issue(f, rk, rv);
+        }
         if constexpr (MULTI) {
           const int qs = s_ppre[b], rb = kSegRows * chunk_of_info(info);
           const bool ld = (info & (kInfoFirst | kInfoStart)) != 0;
