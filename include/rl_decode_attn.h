@@ -146,7 +146,7 @@ rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t handle, int32_t batch, 
  *   - packed (at least two members fit the 16 rows of one MFMA tile: 2G <= 16,
  *     group_size >= 2, batch <= 4096, max_pages_per_seq <= 32767, and the prompt
  *     bytes packing reads again, (packs per group - 1) * groups * Hkv *
- *     prompt_pages_hint * 32 * head_dim * bytes(kv), below 200 MiB): one kernel.
+ *     prompt_pages_hint * 32 * head_dim * bytes(kv), below 240 MiB): one kernel.
  *     Up to min(7, 16/G) consecutive members of a group form a pack whose rows
  *     share one tile; the pack's segment streams the prompt pages once with every
  *     member's rows, then each member's own pages with only its rows unmasked.

@@ -27,7 +27,7 @@ namespace {
 
 constexpr size_t kAlign = 256;
 constexpr int kDefaultWsRanges = 1024;   // default work ranges = CU count (256 on MI355X)
-constexpr int64_t kPackedExtraBytes = 200ll << 20;   // grouped runs: packed below this many re-read prompt bytes
+constexpr int64_t kPackedExtraBytes = 240ll << 20;   // grouped runs: packed below this many re-read prompt bytes
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -253,8 +253,9 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32
   // Packed runs read each prompt page once per pack, the prompt pass once per group
   // at a fixed cost (a second launch, its merge).  With the caller's prompt length
   // in hand, the prompt pass is taken once the extra prompt bytes of packing exceed
-  // kPackedExtraBytes (measured: equal times at 2048-token prompts on the GRPO
-  // workload, 32 groups of 8, two KV heads, G = 6).
+  // kPackedExtraBytes (measured on the GRPO workload, 32 groups of 8, two KV heads,
+  // G = 6: packed 6% faster at 2048-token prompts, 14% slower at 4096; equal
+  // times near 2600).
   const int64_t page_bytes = 2 * (int64_t)rlda::kPage * c.head_dim * elem_bytes(c.kv_dtype);
   const int64_t extra = prompt_pages_hint > 0 ? (int64_t)(per_group - 1) * ngroups * c.num_kv_heads *
                                                     prompt_pages_hint * page_bytes
