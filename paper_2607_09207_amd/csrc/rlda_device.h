@@ -46,6 +46,20 @@ __device__ __forceinline__ f32x2 fp8x2_to_f32(uint32_t w, bool hi_half) {
   return hi_half ? __builtin_amdgcn_cvt_pk_f32_fp8(w, true) : __builtin_amdgcn_cvt_pk_f32_fp8(w, false);
 }
 
+#ifndef RLDA_FP8_DIRECT
+#define RLDA_FP8_DIRECT 1
+#endif
+constexpr bool kFp8Direct = RLDA_FP8_DIRECT;   // fp8 -> bf16 operands in one conversion per pair
+
+// Two e4m3 values (bytes 0, 1, or 2, 3 with hi_half) to a bf16 pair, low half first.
+// Every e4m3 value is a bf16 value, and the scale is one, so the conversion is exact.
+__device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t w, bool hi_half) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 v = hi_half ? __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, true)
+                           : __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, false);
+  return __builtin_bit_cast(uint32_t, v);
+}
+
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   bf16x2 v = {(__bf16)lo, (__bf16)hi};

@@ -370,6 +370,11 @@ struct Mfma {
     } else {
       const u32x4 w = f.k[s >> 1];
       const uint32_t lo = w[2 * (s & 1)], hi = w[2 * (s & 1) + 1];
+      if constexpr (kFp8Direct) {   // fp8 pairs straight to bf16 pairs (unit scale: exact)
+        u32x4 o = {fp8x2_to_bf16x2(lo, false), fp8x2_to_bf16x2(lo, true), fp8x2_to_bf16x2(hi, false),
+                   fp8x2_to_bf16x2(hi, true)};
+        return __builtin_bit_cast(bf16x8, o);
+      }
       f32x2 a = __builtin_amdgcn_cvt_pk_f32_fp8(lo, false);
       f32x2 b = __builtin_amdgcn_cvt_pk_f32_fp8(lo, true);
       f32x2 c = __builtin_amdgcn_cvt_pk_f32_fp8(hi, false);
@@ -402,6 +407,19 @@ struct Mfma {
           hi = (w2 >> 16) | (w3 & 0xFFFF0000u);
         }
         vo.a[t] = __builtin_bit_cast(s16x4, u32x2{lo, hi});
+      }
+    } else if constexpr (kFp8Direct) {
+#pragma unroll
+      for (int u = 0; u < DT / 2; ++u) {   // element pair (2u, 2u+1) of each row
+        // Bytes (row 0, row 1) of elements 2u and 2u+1 in one word, then each pair to
+        // bf16: word 0 of the operands of tiles 2u and 2u+1; rows 2, 3 give word 1.
+        const int sh = (u & 1) * 16;
+        const uint32_t w0 = word_of(f.v[0], u >> 1) >> sh, w1 = word_of(f.v[1], u >> 1) >> sh;
+        const uint32_t w2 = word_of(f.v[2], u >> 1) >> sh, w3 = word_of(f.v[3], u >> 1) >> sh;
+        const uint32_t x01 = __builtin_amdgcn_perm(w1, w0, 0x05010400u);   // r0e0 r1e0 r0e1 r1e1
+        const uint32_t x23 = __builtin_amdgcn_perm(w3, w2, 0x05010400u);
+        vo.a[2 * u] = __builtin_bit_cast(s16x4, u32x2{fp8x2_to_bf16x2(x01, false), fp8x2_to_bf16x2(x23, false)});
+        vo.a[2 * u + 1] = __builtin_bit_cast(s16x4, u32x2{fp8x2_to_bf16x2(x01, true), fp8x2_to_bf16x2(x23, true)});
       }
     } else {
 #pragma unroll
