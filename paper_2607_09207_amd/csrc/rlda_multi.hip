@@ -285,9 +285,14 @@ void multi_query_kernel(const Params p) {
           uint32_t w[8];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const f32x2 a = fp8x2_to_f32(stg[set][h][k][e], false), bb = fp8x2_to_f32(stg[set][h][k][e], true);
-            w[2 * e] = pack_bf16(a[0], a[1]);
-            w[2 * e + 1] = pack_bf16(bb[0], bb[1]);
+            if constexpr (kFp8Direct) {
+              w[2 * e] = fp8x2_to_bf16x2(stg[set][h][k][e], false);
+              w[2 * e + 1] = fp8x2_to_bf16x2(stg[set][h][k][e], true);
+            } else {
+              const f32x2 a = fp8x2_to_f32(stg[set][h][k][e], false), bb = fp8x2_to_f32(stg[set][h][k][e], true);
+              w[2 * e] = pack_bf16(a[0], a[1]);
+              w[2 * e + 1] = pack_bf16(bb[0], bb[1]);
+            }
           }
           *(u32x4*)(rowp + 32 * c) = u32x4{w[0], w[1], w[2], w[3]};
           *(u32x4*)(rowp + 32 * c + 16) = u32x4{w[4], w[5], w[6], w[7]};
