@@ -13,6 +13,9 @@ LIB = os.path.join(HERE, "librl_decode_attn.so")
 SOURCES = [os.path.join(CSRC, "rlda_kernels.hip"), os.path.join(CSRC, "rlda_multi.hip"),
            os.path.join(CSRC, "rlda_host.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+# Read-bandwidth reference kernels (bench support, not the attention path).
+PROBE_SOURCES = [os.path.join(CSRC, "hbm_probe.hip")]
+PROBE_LIB = os.path.join(HERE, "libhbm_probe.so")
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -23,9 +26,9 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
+def build(verbose: bool = False, out: str = LIB, defines=(), sources=None) -> str:
     tmp = out + ".tmp%d" % os.getpid()
-    cmd = [HIPCC] + FLAGS + ["-D" + d for d in defines] + SOURCES + ["-o", tmp]
+    cmd = [HIPCC] + FLAGS + ["-D" + d for d in defines] + (sources or SOURCES) + ["-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -47,5 +50,13 @@ def device_asm(out_path: str, source: int = 0) -> str:
     return out_path
 
 
+def build_all(verbose: bool = False) -> None:
+    """The attention library and the read-bandwidth probe library."""
+    build(verbose=verbose)
+    build(verbose=verbose, out=PROBE_LIB, sources=PROBE_SOURCES)
+
+
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    build_all(verbose="-v" in sys.argv)
+    print(LIB)
+    print(PROBE_LIB)

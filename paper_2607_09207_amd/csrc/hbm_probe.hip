@@ -1,0 +1,131 @@
+// Achievable HBM read rate on gfx950: two read-only kernels that set the ceiling
+// a bandwidth-bound kernel is measured against.  Not part of the attention path;
+// the bench loads this library next to the attention library and reports the best
+// rate each kernel reaches over a few launch shapes.
+//
+//   stream read  - a contiguous buffer read once, 16 bytes per lane per load,
+//                  U loads in flight per lane, non-temporal (the data is not reused);
+//   tile gather  - the decode kernel's access pattern without its arithmetic: a list
+//                  of (K, V) tile pairs at byte offsets into two pools (one pair per
+//                  (sequence, KV head, page) of a workload, in the order the decode
+//                  kernel streams them), cut into equal contiguous shares, one per
+//                  wave, with U tile pairs in flight per wave.
+// Both fold every loaded word into a per-lane value and store it only when it
+// equals a sentinel, so the loads cannot be removed and almost nothing is written.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "hbm_probe.h"
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+constexpr uint32_t kSentinel = 0x9E3779B9u;
+
+__device__ __forceinline__ uint32_t fold(u32x4 v) { return v[0] ^ v[1] ^ v[2] ^ v[3]; }
+
+template <int U>
+__global__ void stream_read_kernel(const u32x4* __restrict__ buf, uint64_t n16, uint32_t* __restrict__ sink) {
+  const uint64_t nthreads = (uint64_t)gridDim.x * blockDim.x;
+  uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  uint32_t acc = 0;
+  // Full rounds: U loads per lane, all addresses in range.
+  for (; i + (U - 1) * nthreads < n16; i += U * nthreads) {
+    u32x4 v[U];
+#pragma unroll
+    for (int k = 0; k < U; ++k) v[k] = __builtin_nontemporal_load(buf + i + k * nthreads);
+#pragma unroll
+    for (int k = 0; k < U; ++k) acc ^= fold(v[k]);
+  }
+  for (; i < n16; i += nthreads) acc ^= fold(__builtin_nontemporal_load(buf + i));
+  if (acc == kSentinel) sink[blockIdx.x] = acc;
+}
+
+// Wave w of the grid reads entries [w*n/W, (w+1)*n/W) of the offset list: for each,
+// the K tile and the V tile of `tile_bytes` at that byte offset.  Lane l loads bytes
+// [16 l, 16 l + 16) of each 1 KiB quarter-row group, so one load instruction of the
+// wave covers 1 KiB contiguous.
+template <int U>
+__global__ void tile_gather_kernel(const char* __restrict__ k, const char* __restrict__ v,
+                                   const int64_t* __restrict__ off, int64_t n, int tile_bytes,
+                                   uint32_t* __restrict__ sink) {
+  const int lane = threadIdx.x & 63;
+  const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
+  const int64_t w = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  const int64_t e0 = w * n / waves, e1 = (w + 1) * n / waves;
+  const int per = tile_bytes / 1024;   // 1 KiB load instructions per tile
+  uint32_t acc = 0;
+  for (int64_t e = e0; e < e1; e += U) {
+    u32x4 kv[U][2][4];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool ok = e + u < e1;
+      const int64_t o = ok ? off[e + u] : off[e0];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int64_t b = o + (int64_t)c * 1024 + lane * 16;
+        const bool in = ok && c < per;
+        kv[u][0][c] = in ? __builtin_nontemporal_load((const u32x4*)(k + b)) : u32x4{0, 0, 0, 0};
+        kv[u][1][c] = in ? __builtin_nontemporal_load((const u32x4*)(v + b)) : u32x4{0, 0, 0, 0};
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc ^= fold(kv[u][0][c]) ^ fold(kv[u][1][c]);
+  }
+  if (acc == kSentinel) sink[blockIdx.x] = acc;
+}
+
+template <int U>
+int launch_stream(const void* buf, uint64_t n16, uint32_t* sink, int blocks, int threads, hipStream_t st) {
+  hipLaunchKernelGGL((stream_read_kernel<U>), dim3(blocks), dim3(threads), 0, st, (const u32x4*)buf, n16, sink);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+template <int U>
+int launch_gather(const void* k, const void* v, const int64_t* off, int64_t n, int tile_bytes, uint32_t* sink,
+                  int blocks, int threads, hipStream_t st) {
+  hipLaunchKernelGGL((tile_gather_kernel<U>), dim3(blocks), dim3(threads), 0, st, (const char*)k, (const char*)v,
+                     off, n, tile_bytes, sink);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+bool shape_ok(int blocks, int threads) {
+  return blocks >= 1 && blocks <= (1 << 20) && threads >= 64 && threads <= 1024 && threads % 64 == 0;
+}
+
+}  // namespace
+
+extern "C" {
+
+int hbm_probe_stream_read(const void* buf, uint64_t bytes, uint32_t* sink, int blocks, int threads, int unroll,
+                          void* stream) {
+  if (!buf || !sink || bytes % 16 || !shape_ok(blocks, threads)) return -1;
+  const hipStream_t st = (hipStream_t)stream;
+  const uint64_t n16 = bytes / 16;
+  switch (unroll) {
+    case 1: return launch_stream<1>(buf, n16, sink, blocks, threads, st);
+    case 2: return launch_stream<2>(buf, n16, sink, blocks, threads, st);
+    case 4: return launch_stream<4>(buf, n16, sink, blocks, threads, st);
+    case 8: return launch_stream<8>(buf, n16, sink, blocks, threads, st);
+    case 16: return launch_stream<16>(buf, n16, sink, blocks, threads, st);
+  }
+  return -1;
+}
+
+int hbm_probe_tile_gather(const void* k_pool, const void* v_pool, const int64_t* tile_offsets, int64_t ntiles,
+                          int tile_bytes, uint32_t* sink, int blocks, int threads, int depth, void* stream) {
+  if (!k_pool || !v_pool || !sink || ntiles < 0 || (ntiles > 0 && !tile_offsets)) return -1;
+  if (tile_bytes < 1024 || tile_bytes > 4096 || tile_bytes % 1024 || !shape_ok(blocks, threads)) return -1;
+  const hipStream_t st = (hipStream_t)stream;
+  switch (depth) {
+    case 1: return launch_gather<1>(k_pool, v_pool, tile_offsets, ntiles, tile_bytes, sink, blocks, threads, st);
+    case 2: return launch_gather<2>(k_pool, v_pool, tile_offsets, ntiles, tile_bytes, sink, blocks, threads, st);
+    case 3: return launch_gather<3>(k_pool, v_pool, tile_offsets, ntiles, tile_bytes, sink, blocks, threads, st);
+    case 4: return launch_gather<4>(k_pool, v_pool, tile_offsets, ntiles, tile_bytes, sink, blocks, threads, st);
+  }
+  return -1;
+}
+
+}  // extern "C"

@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <mutex>
 #include <new>
 
@@ -73,6 +74,13 @@ int cu_count(int dev) {
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Counter tags: one per call, cycling over [1, kMaxCallTag] across the process, so
+// a segment counter left by a call that did not complete (or never zeroed) is
+// told apart from this call's count.
+std::atomic<uint32_t> g_call_seq{0};
+
+uint32_t next_call_tag() { return g_call_seq.fetch_add(1, std::memory_order_relaxed) % rlda::kMaxCallTag + 1; }
 
 }  // namespace
 
@@ -220,6 +228,7 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32
   p.out = out;
   p.flags = (uint32_t*)(ws + wl.flags);
   p.counters = (uint32_t*)(ws + wl.counters);
+  p.call_tag = next_call_tag();
   p.part_ml = (float*)(ws + wl.part_ml);
   p.part_acc = (float*)(ws + wl.part_acc);
   p.part_rows = h->group;
@@ -459,6 +468,7 @@ rlda_status rl_decode_attn_run_multi(rl_decode_attn_t h, int32_t batch, int32_t 
     if (ranges < 1) ranges = 1;
     p.nranges = ranges;
     p.counters = (uint32_t*)(ws + wl.counters);
+    p.call_tag = next_call_tag();
     p.part_ml = (float*)(ws + wl.part_ml);
     p.part_acc = (float*)(ws + wl.part_acc);
     if (rlda::launch_decode_rows(h->kind, c.head_dim, tiles, p, stream, event_begin, event_end) != hipSuccess)

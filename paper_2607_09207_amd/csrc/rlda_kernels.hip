@@ -31,12 +31,13 @@
 //      wave.  The cut pieces (at most 2 per wave) are merged through LDS.  A piece
 //      of a segment that is split across workgroups stores its unnormalised
 //      partial with device-scope (sc1) stores, which write through the XCD's L2;
-//      after they complete, the workgroup bumps the segment's counter.  The
-//      workgroup that completes the count reads every piece of the segment with
-//      device-scope loads, merges them in piece order with log-sum-exp weights,
-//      writes the output and resets the counter.  No workgroup waits for another,
-//      and no device-scope fence (a whole-L2 writeback and invalidate per XCD) is
-//      issued.
+//      after they complete, the workgroup bumps the segment's counter (tagged
+//      with the call, so a counter another call left behind is detected and
+//      restarted).  The workgroup that completes the count reads every piece of
+//      the segment with device-scope loads, merges them in piece order with
+//      log-sum-exp weights, writes the output and resets the counter.  No
+//      workgroup waits for another, and no device-scope fence (a whole-L2
+//      writeback and invalidate per XCD) is issued.
 // fp8 (OCP E4M3FN) caches are converted exactly to bf16 for the MFMA; the K
 // scale multiplies the scores and the V scale multiplies P.  fp32 caches use a
 // VALU path.
@@ -150,6 +151,31 @@ struct PartialRsrc {
     return {make_rsrc_uni(p.part_acc, slots * D * 4u), make_rsrc_uni(p.part_ml, slots * 8u)};
   }
 };
+
+static_assert(kMaxRanges < (1 << kCounterCountBits), "piece counts must fit the counter's count field");
+
+// Count one finished piece of a split segment in its counter word; returns the
+// pieces of this call counted so far, this one included.  A word holding another
+// call's tag with a nonzero count was left by a call that never completed on this
+// workspace, or the workspace was not zero-filled: the count restarts from this
+// piece (so the result is unaffected) and kFlagStaleCounter is raised.  Lock-free:
+// a failed compare-and-swap means another piece's succeeded.
+__device__ __forceinline__ uint32_t count_piece(uint32_t* ctr, uint32_t tag, uint32_t* flags) {
+  constexpr uint32_t kMask = (1u << kCounterCountBits) - 1;
+  uint32_t old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  uint32_t nw;
+  bool stale;
+  for (;;) {
+    const bool mine = (old >> kCounterCountBits) == tag;
+    stale = !mine && old != 0;
+    nw = mine ? old + 1 : (tag << kCounterCountBits) | 1u;
+    const uint32_t prev = atomicCAS(ctr, old, nw);
+    if (prev == old) break;
+    old = prev;
+  }
+  if (stale) atomicOr(flags, kFlagStaleCounter);
+  return nw & kMask;
+}
 
 // Online log-sum-exp merge of one partial (mj, lj, v[]) into (M, Ls, o[]).
 template <int N>
@@ -1263,7 +1289,9 @@ void decode_attention_kernel(const Params p) {
     const int64_t seg_start = (int64_t)Hs * pre_b + (int64_t)g * nb;
     const uint32_t npieces = (uint32_t)(owner_of(cost_of(seg_start + nb - 1, b, g), Wn, C) -
                                         owner_of(cost_of(seg_start, b, g), Wn, C) + 1);
-    s_last[tid] = (atomicAdd(p.counters + sgi, 1u) + 1u == npieces);
+    const uint32_t got = count_piece(p.counters + sgi, p.call_tag, p.flags);
+    if (got > npieces) atomicOr(p.flags, kFlagStaleCounter);   // more pieces than the segment has
+    s_last[tid] = (got == npieces);
   }
   __syncthreads();
   for (int i = 0; i < nhand; ++i) {
@@ -1428,7 +1456,7 @@ void prompt_kernel(const Params p) {
                                             kDeviceScope);
     __builtin_amdgcn_s_waitcnt(0);   // this wave's device-scope stores have completed
     __syncthreads();                 // ... and every other wave's
-    if (tid == 0) s_min = (atomicAdd(p.counters + job, 1u) + 1u == (uint32_t)S);
+    if (tid == 0) s_min = (count_piece(p.counters + job, p.call_tag, p.flags) == (uint32_t)S);
     __syncthreads();
     if (!s_min) return;
     if (tid == 0) atomicExch(p.counters + job, 0u);

@@ -27,6 +27,15 @@ constexpr int kMaxRowsQLen = 16;   // ... and at most 16 rows per sequence (a fu
 constexpr uint32_t kFlagBadPage = 1u;
 constexpr uint32_t kFlagBadLen = 2u;
 constexpr uint32_t kFlagPrefixClamped = 4u;
+constexpr uint32_t kFlagStaleCounter = 8u;   // a segment counter held another call's count
+
+// Segment counters: the high kCounterTagBits bits of a counter word hold the tag of
+// the call counting in it, the low bits the pieces counted so far (at most
+// kMaxRanges).  A word that is 0, or carries another call's tag, starts a fresh
+// count; 0 is what every merge leaves behind.  Tags run over [1, kMaxCallTag].
+constexpr int kCounterCountBits = 13;
+constexpr int kCounterTagBits = 32 - kCounterCountBits;
+constexpr uint32_t kMaxCallTag = (1u << kCounterTagBits) - 2;   // all-ones is never a tag
 
 struct Params {
   const void* q;               // [batch][Hq][D]
@@ -40,7 +49,8 @@ struct Params {
   float* part_acc;             // [2 * nranges][part_rows][D]  unnormalised partial outputs
   float* part_ml;              // [2 * nranges][part_rows][2]  (running max in log2 units, sum)
   int32_t part_rows;           // query rows per (sequence, KV head) segment: G, or n_max * G for multi-token rows
-  uint32_t* counters;          // [max_batch * Hkv] finished pieces per split segment; zero between runs
+  uint32_t* counters;          // [max_batch * Hkv * 4] (call tag, finished pieces) per split segment
+  uint32_t call_tag;           // this call's counter tag, in [1, kMaxCallTag]
   uint32_t* flags;             // contract-violation bits
   int64_t stride_page;         // bytes
   int64_t stride_head;         // bytes

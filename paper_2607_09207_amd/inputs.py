@@ -453,6 +453,18 @@ def make_custom(seq_lens: Sequence[int], num_q_heads: int, num_kv_heads: int, he
                           shared_prefix_tokens=ptok, group_size=group, poison=poison)
 
 
+def spread_sequences(seq_lens) -> list:
+    """Indices of sequences spread over the length order, for checks on whole
+    sequences of a large workload: the shortest, the longest, the middle one of
+    every tenth of the order and the first of every quarter (16 of 64)."""
+    order = np.argsort(np.asarray(seq_lens), kind="stable")
+    B = len(order)
+    if B == 0:
+        return []
+    ranks = {0, B - 1} | {int((k + 0.5) * B / 10) for k in range(10)} | {min(B - 1, int(j * B / 4) + 1) for j in range(4)}
+    return sorted(int(order[r]) for r in ranks)
+
+
 def to_page_slot_head(w: Workload) -> Workload:
     """Same logical cache re-laid out as [NP][P][Hkv][d] (strides change, values do not)."""
     assert w.layout == "page_head_slot"

@@ -34,6 +34,45 @@ def test_every_declared_function_is_exported(lib):
         assert hasattr(lib, n), n
 
 
+def test_probe_library_exports_its_declared_functions():
+    """The read-bandwidth reference kernels (include/hbm_probe.h) load and export
+    every declared function; argument errors return -1 before any HIP call."""
+    from paper_2607_09207_amd import build, probe
+    if not os.path.exists(probe.LIB_PATH):
+        build.build(out=build.PROBE_LIB, sources=build.PROBE_SOURCES)
+    plib = probe.load()
+    txt = open(os.path.join(ROOT, "include", "hbm_probe.h")).read()
+    names = sorted(set(re.findall(r"^int\s+(hbm_probe_\w+)\s*\(", txt, re.M)))
+    assert names == ["hbm_probe_stream_read", "hbm_probe_tile_gather"]
+    for n in names:
+        assert hasattr(plib, n), n
+    sink = ctypes.c_void_p(256)
+    assert plib.hbm_probe_stream_read(None, 1024, sink, 1, 256, 8, None) == -1          # null buffer
+    assert plib.hbm_probe_stream_read(ctypes.c_void_p(256), 1000, sink, 1, 256, 8, None) == -1   # not a multiple of 16
+    assert plib.hbm_probe_stream_read(ctypes.c_void_p(256), 1024, sink, 1, 100, 8, None) == -1   # threads % 64
+    assert plib.hbm_probe_stream_read(ctypes.c_void_p(256), 1024, sink, 1, 256, 3, None) == -1   # unroll
+    assert plib.hbm_probe_tile_gather(ctypes.c_void_p(256), ctypes.c_void_p(256), None, 4, 4096, sink, 1, 256, 2,
+                                      None) == -1                                              # no offsets
+    assert plib.hbm_probe_tile_gather(ctypes.c_void_p(256), ctypes.c_void_p(256), ctypes.c_void_p(256), 4, 1000,
+                                      sink, 1, 256, 2, None) == -1                             # tile size
+    assert plib.hbm_probe_tile_gather(ctypes.c_void_p(256), ctypes.c_void_p(256), ctypes.c_void_p(256), 4, 4096,
+                                      sink, 1, 256, 5, None) == -1                             # depth
+
+
+def test_tile_offsets_follow_the_stream_order():
+    import numpy as np
+    from paper_2607_09207_amd import inputs as I, probe
+    w = I.make_custom([17, 0, 40], 8, 2, 128, seed=3)
+    off = probe.tile_offsets(w)
+    sp, sh = w.strides()[0] * 2, w.strides()[1] * 2
+    want = []
+    for b, L in enumerate(w.seq_lens):
+        n = (int(L) + 15) // 16
+        for g in range(2):
+            want += [int(w.block_table[b, j]) * sp + g * sh for j in range(n)]
+    assert off.tolist() == want and off.dtype == np.int64
+
+
 def cfg(**kw):
     c = _abi.Config()
     base = dict(num_q_heads=28, num_kv_heads=4, head_dim=128, page_size=16, max_batch=64, max_pages_per_seq=1024,

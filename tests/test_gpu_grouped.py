@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 from paper_2607_09207_amd import inputs as I
-from test_gpu_parity import TOL, assert_close, handle_for, log, sample_rows
+from test_gpu_parity import TOL, assert_close, handle_for, log
 
 pytestmark = pytest.mark.gpu
 
@@ -149,18 +149,17 @@ def test_grouped_runs_are_bitwise_deterministic_and_reuse_the_workspace(torch_cu
     assert_close(outs[1], oracle.run(w2), "bf16", "reuse w2")
 
 
-def test_grpo_workload_full_size_grouped(torch_cuda):
+@pytest.mark.parametrize("hint", [-1, 1 << 20], ids=["packed", "prompt-pass"])
+def test_grpo_workload_full_size_grouped(torch_cuda, hint):
+    """The GRPO workload through the shared-prompt entry point, both forms, every
+    output element against the fp64 oracle."""
     w = I.make_workload("grpo_shared_prefix_bf16")
     ng = w.batch // w.group_size
-    got, flags = run_grouped(torch_cuda, w, w.group_size, [w.shared_prefix_tokens // 16] * ng, tag="grpo full")
+    got, flags = run_grouped(torch_cuda, w, w.group_size, [w.shared_prefix_tokens // 16] * ng, hint=hint,
+                             tag=f"grpo full hint={hint}")
     assert flags == 0
     assert np.all(np.isfinite(got))
-    mask = sample_rows(w)
-    # also every member of one group, so the shared prompt is checked across a whole group
-    mask[8:16] = 1
-    want = oracle.run(w, batch_mask=mask)
-    rows = np.nonzero(mask)[0]
-    assert_close(got[rows], want[rows], "bf16", "grpo full grouped")
+    assert_close(got, oracle.run(w), "bf16", f"grpo full grouped hint={hint} (all {got.size} outputs)")
 
 
 def test_grouped_beyond_the_packed_batch_limit(torch_cuda):

@@ -103,17 +103,14 @@ def test_rows_path_more_rows_than_tokens_zeroes_rows_before_position_zero(torch_
                  "rows > tokens: other sequences")
 
 
-def test_full_size_verify_workload_sampled(torch_cuda):
+def test_full_size_verify_workload(torch_cuda):
+    """Every output of the draft-verification workload (64 sequences x 4 rows) on the
+    decode-stream path against the fp64 oracle (0.3 s of oracle time)."""
     w = I.make_workload("verify_gqa_bf16")
     got, flags = run_multi(torch_cuda, w, tag="verify_gqa_bf16", max_q_len=4)
     assert flags == 0
     assert np.all(np.isfinite(got))
-    pick = sorted({0, w.batch // 2, int(np.argmax(w.seq_lens)), int(np.argmin(w.seq_lens))})
-    mask = np.zeros(w.batch, np.uint8)
-    mask[pick] = 1
-    want = oracle.run_multi(w, batch_mask=mask)
-    rows = np.concatenate([np.arange(w.q_start[b], w.q_start[b + 1]) for b in pick])
-    assert_close(got[rows], want[rows], "bf16", f"verify_gqa_bf16 sampled sequences {pick}")
+    assert_close(got, oracle.run_multi(w), "bf16", f"verify_gqa_bf16 (all {got.size} outputs)")
 
 
 def test_rows_path_is_bitwise_deterministic(torch_cuda):

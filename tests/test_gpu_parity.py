@@ -239,6 +239,36 @@ def test_workspace_reuse_with_smaller_batch(torch_cuda):
         assert_close(got, oracle.run(w), "bf16", "reuse")
 
 
+@pytest.mark.parametrize("pattern", [0xFFFFFFFF, 0xFFFFE001], ids=["all-ones", "stale-count-1"])
+def test_dirty_workspace_counters_are_flagged_and_restarted(torch_cuda, pattern):
+    """A workspace that was never zero-filled: every word (counters and partial slots)
+    holds `pattern` except the flag word.  0xFFFFE001 is a count of one piece under a
+    tag no call uses, the case a plain piece count would merge early.  The split
+    segments' counters restart, the output is the oracle's, and flag bit 3 reports
+    the stale counters; a second call on the same workspace finds them clean."""
+    torch = torch_cuda
+    w = I.make_custom([3000, 20, 1700, 9, 800, 5000, 1], 28, 4, 128, q_dtype="bf16", kv_dtype="bf16", seed=31)
+    h = handle_for(w, ranges=61)
+    t = I.to_torch(w, "cuda")
+    ws = torch.empty(h.workspace_bytes + 256, dtype=torch.uint8, device="cuda")
+    off = (ws.data_ptr() + 255) // 256 * 256 - ws.data_ptr()
+    words = ws[off:off + (h.workspace_bytes // 4) * 4].view(torch.int32)
+    words.fill_(np.int32(np.uint32(pattern).view(np.int32)))
+    words[0] = 0   # the flag word
+    args = (t["q"], t["k_cache"], t["v_cache"], t["block_table"], t["seq_lens"])
+    log(f"dirty workspace pattern={pattern:#010x}, 61 work ranges")
+    first = h(*args, workspace=ws).clone()
+    torch.cuda.synchronize()
+    flags = h.read_flags(workspace=ws)
+    assert flags == 8, f"flags {flags:#x}"
+    assert_close(first.double().cpu().numpy(), oracle.run(w), "bf16", "dirty workspace")
+    words[0] = 0
+    second = h(*args, workspace=ws)
+    torch.cuda.synchronize()
+    assert h.read_flags(workspace=ws) == 0
+    assert torch.equal(first, second)
+
+
 def test_contract_violations_raise_flags_without_faulting(torch_cuda):
     torch = torch_cuda
     w = I.make_custom([40, 300, 20], 8, 2, 128, q_dtype="bf16", kv_dtype="bf16", seed=16)
@@ -257,31 +287,20 @@ def test_contract_violations_raise_flags_without_faulting(torch_cuda):
     assert_close(got[:2], oracle.run(w)[:2], "bf16", "bad-len other rows")
 
 
-# ------------------------------------------------------------------ full-size workloads, sampled compare
-
-def sample_rows(w, k_long=3, k_short=2, k_rand=3, seed=0):
-    L = w.seq_lens
-    order = np.argsort(L, kind="stable")
-    rng = np.random.default_rng(seed)
-    pick = set(order[-k_long:].tolist()) | set(order[:k_short].tolist())
-    pick |= set(rng.choice(len(L), size=min(k_rand, len(L)), replace=False).tolist())
-    mask = np.zeros(len(L), np.uint8)
-    mask[sorted(pick)] = 1
-    return mask
-
+# ------------------------------------------------------------------ full-size workloads, every output
 
 @pytest.mark.parametrize("name", I.WORKLOAD_ORDER)
 def test_full_size_workload(torch_cuda, name):
+    """Every output element of every full-size workload against the fp64 oracle
+    (the largest, staleness_mix_bf16, is 512 x 64 x 128 outputs over 2.2M cached
+    tokens: about 1.5 s of oracle time on 16 cores)."""
     log(f"generating {name}")
     w = I.make_workload(name)
     got, flags = gpu_run(torch_cuda, w, tag=f"full {name}")
     assert flags == 0
     assert np.all(np.isfinite(got))
-    mask = None if w.batch <= 8 else sample_rows(w)
-    log(f"oracle on {'all' if mask is None else int(mask.sum())} sequences")
-    want = oracle.run(w, batch_mask=mask)
-    rows = np.arange(w.batch) if mask is None else np.nonzero(mask)[0]
-    assert_close(got[rows], want[rows], w.kv_dtype, f"full {name}")
+    log(f"oracle on all {w.batch} sequences")
+    assert_close(got, oracle.run(w), w.kv_dtype, f"full {name} (all {got.size} outputs)")
 
 
 def test_functional_api_and_profiled_events(torch_cuda):
