@@ -40,3 +40,61 @@ def test_batch_plans_are_seeded_and_bounded():
     cap = C.MAX_KV_BYTES // C.kv_bytes_per_token(cfg)
     assert all(x.min() >= 1 and x.sum() <= cap + len(x) for x in a)
     assert not all(np.array_equal(x, y) for x, y in zip(a, C.batch_plan(2, cfg)))
+
+
+def brute_max_pieces(lens, Hs, ranges, S=2, P=16):
+    """Price every (sequence, KV head, page) position one by one, give each the share
+    whose cost interval holds it, and count the distinct shares of every segment."""
+    n = [(L + P - 1) // P for L in lens]
+    costs, segs = [], []
+    ne = 0
+    p = 0
+    for b, nb in enumerate(n):
+        for g in range(Hs if nb else 0):
+            for j in range(nb):
+                costs.append(p + S * (Hs * ne + g + 1))
+                segs.append((b, g))
+                p += 1
+        ne += nb > 0
+    T = p
+    if T == 0:
+        return 0
+    C = Hs * (sum(n) + S * ne)
+    W = min(ranges, T)
+    bounds = [u * C // W for u in range(W + 1)]
+    shares = {}
+    for c, s in zip(costs, segs):
+        u = max(k for k in range(W) if bounds[k] <= c)
+        shares.setdefault(s, set()).add(u)
+    return max(len(v) for v in shares.values())
+
+
+def test_max_pieces_matches_a_position_by_position_split():
+    rng = np.random.default_rng(3)
+    cases = [([35000] + [10] * 7, 4, 64), ([2000] * 16, 4, 64), ([0, 5, 0, 900], 2, 37), ([1], 8, 256),
+             (list(rng.integers(0, 3000, size=12)), 4, 100), (list(rng.integers(0, 400, size=30)), 8, 256)]
+    for lens, Hs, ranges in cases:
+        assert C.max_pieces(lens, Hs, ranges) == brute_max_pieces(lens, Hs, ranges), (lens, Hs, ranges)
+    assert C.max_pieces([0, 0], 4, 256) == 0
+
+
+def test_extended_fit_recovers_a_merge_term():
+    rng = np.random.default_rng(1)
+    X = np.array([[1.0, b, h, m] for b, h, m in zip(rng.integers(1, 512, 80), rng.integers(1000, 2_000_000, 80),
+                                                       rng.integers(1, 200, 80))], np.float64)
+    true = np.array([15e-6, 20e-9, 300e-12, 90e-9])
+    y = X @ true
+    assert np.allclose(C.fit(X, y), true, rtol=1e-3)
+
+
+def test_load_fit_rejects_summaries_of_other_kernel_sources(tmp_path):
+    good = tmp_path / "fit.md"
+    good.write_text(f"- kernel_source_hash: `{C.kernel_source_hash()}`\n"
+                    "- fit paper demo: 1.0e-05 2.0e-08 3.0e-10\n- fit extended demo: 1 2 3 4\n")
+    assert np.allclose(C.load_fit(str(good), "demo"), [1e-5, 2e-8, 3e-10])
+    assert len(C.load_fit(str(good), "demo", "extended")) == 4
+    assert C.load_fit(str(good), "other") is None
+    stale = tmp_path / "stale.md"
+    stale.write_text("- kernel_source_hash: `0000000000000000`\n- fit paper demo: 1 2 3\n")
+    assert C.load_fit(str(stale), "demo") is None
+    assert C.load_fit(str(tmp_path / "absent.md"), "demo") is None
