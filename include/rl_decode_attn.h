@@ -57,7 +57,8 @@ typedef enum {
   RLDA_ERR_UNSUPPORTED = -2,   /* valid request outside the built kernel set */
   RLDA_ERR_HIP = -3,           /* a HIP runtime call or a launch failed */
   RLDA_ERR_WORKSPACE = -4,     /* workspace missing or smaller than required */
-  RLDA_ERR_ALLOC = -5          /* host allocation for the handle failed */
+  RLDA_ERR_ALLOC = -5,         /* host allocation for the handle failed */
+  RLDA_ERR_SCRATCH = -6        /* beyond the static scratch of rl_decode_attn_run_noalloc */
 } rlda_status;
 
 typedef struct rlda_handle* rl_decode_attn_t;
@@ -140,6 +141,29 @@ rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t handle, int32_t batch, 
                                         const int32_t* seq_lens, void* out, void* workspace,
                                         size_t workspace_bytes, void* stream, void* event_begin,
                                         void* event_end);
+
+/*
+ * rl_decode_attn_run without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation).  Same operation, kernel and arguments as rl_decode_attn_run, except:
+ *   - the flags, segment counters and partial results live in a static device
+ *     array of the library (about 4.3 MiB; one copy on each GPU the library runs
+ *     on, held until the process ends), found on the first call on each device;
+ *   - limits of that array: batch * num_kv_heads <= 65536 and head_dim <= 128
+ *     (else RLDA_ERR_SCRATCH, nothing launched), and the work is cut into at most
+ *     256 shares (one per CU on MI355X, the default);
+ *   - flags: NULL, or a caller-owned device uint32_t (4-byte aligned) that receives
+ *     the contract bits of rl_decode_attn_read_flags (OR-ed in; the caller clears
+ *     it).  With NULL they go to a word of the static array that nothing reads.
+ * Nothing in the array needs clearing between calls (every call tags its segment
+ * counters).  Every call on one GPU shares that GPU's array: calls that may
+ * overlap in time (different streams) race on it and must not be issued.
+ * No device memory is allocated or freed; one kernel, asynchronous.
+ */
+rlda_status rl_decode_attn_run_noalloc(rl_decode_attn_t handle, int32_t batch, int32_t num_pages, const void* q,
+                                       const void* k_cache, const void* v_cache, const float* k_scale,
+                                       const float* v_scale, const int32_t* block_table, const int32_t* seq_lens,
+                                       void* out, uint32_t* flags, void* stream);
 
 /*
  * Shared-prompt (GRPO group) variant of rl_decode_attn_run.  GRPO samples a group

@@ -141,6 +141,30 @@ class DecodeAttention:
             _abi.check(self._lib.rl_decode_attn_run_profiled(*args, e0, e1), "rl_decode_attn_run_profiled")
         return out
 
+    def run_noalloc(self, q, k_cache, v_cache, block_table, seq_lens, k_scale=None, v_scale=None, out=None,
+                    flags=None, stream=None, num_pages: Optional[int] = None):
+        """The same attention through rl_decode_attn_run_noalloc, which takes no
+        workspace: its flags, segment counters and partials live in the library's static
+        device array (limits: batch * Hkv <= 65536, head_dim <= 128).  `flags`: None, or
+        a one-element int32 device tensor that receives the contract bits (OR-ed in)."""
+        torch = _torch()
+        B = int(q.shape[0])
+        cfg = self.config
+        if out is None:
+            odt = torch.float32 if cfg.out_dtype == _abi.RLDA_F32 else torch.bfloat16
+            out = torch.empty((B, cfg.num_q_heads, cfg.head_dim), dtype=odt, device=q.device)
+        if stream is None:
+            stream = torch.cuda.current_stream(q.device).cuda_stream
+        elif hasattr(stream, "cuda_stream"):
+            stream = stream.cuda_stream
+        npages = int(k_cache.shape[0]) if num_pages is None else int(num_pages)
+        ptr = lambda t: None if t is None else t.data_ptr()
+        _abi.check(self._lib.rl_decode_attn_run_noalloc(self._h, B, npages, ptr(q), ptr(k_cache), ptr(v_cache),
+                                                        ptr(k_scale), ptr(v_scale), ptr(block_table), ptr(seq_lens),
+                                                        ptr(out), ptr(flags), stream),
+                   "rl_decode_attn_run_noalloc")
+        return out
+
     def multi(self, q, k_cache, v_cache, block_table, seq_lens, q_start, k_scale=None, v_scale=None, out=None,
               workspace=None, stream=None, num_pages: Optional[int] = None, events=None, max_q_len: int = 0):
         """Multi-token queries (rl_decode_attn_run_multi): q [total_q][Hq][d], q_start

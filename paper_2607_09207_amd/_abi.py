@@ -9,11 +9,11 @@ LIB_PATH = os.path.join(HERE, "librl_decode_attn.so")
 
 RLDA_F32, RLDA_BF16, RLDA_FP8_E4M3FN = 0, 1, 2
 STATUS = {0: "RLDA_OK", -1: "RLDA_ERR_INVALID_ARG", -2: "RLDA_ERR_UNSUPPORTED", -3: "RLDA_ERR_HIP",
-          -4: "RLDA_ERR_WORKSPACE", -5: "RLDA_ERR_ALLOC"}
+          -4: "RLDA_ERR_WORKSPACE", -5: "RLDA_ERR_ALLOC", -6: "RLDA_ERR_SCRATCH"}
 
 EXPORTS = ["rl_decode_attn_create", "rl_decode_attn_workspace_size", "rl_decode_attn_run",
            "rl_decode_attn_run_profiled", "rl_decode_attn_run_grouped", "rl_decode_attn_grouped_workspace_size",
-           "rl_decode_attn_append", "rl_decode_attn_run_multi",
+           "rl_decode_attn_append", "rl_decode_attn_run_multi", "rl_decode_attn_run_noalloc",
            "rl_decode_attn_read_flags", "rl_decode_attn_destroy", "rl_decode_attn_strerror"]
 
 
@@ -71,6 +71,8 @@ def load() -> ctypes.CDLL:
         lib.rl_decode_attn_append.restype = ctypes.c_int
         lib.rl_decode_attn_run_multi.argtypes = [vp, i32, i32, i32, i32] + [vp] * 9 + [vp, sz, vp, vp, vp]
         lib.rl_decode_attn_run_multi.restype = ctypes.c_int
+        lib.rl_decode_attn_run_noalloc.argtypes = [vp, i32, i32] + [vp] * 8 + [vp, vp]
+        lib.rl_decode_attn_run_noalloc.restype = ctypes.c_int
         lib.rl_decode_attn_read_flags.argtypes = [vp, vp, vp, ctypes.POINTER(ctypes.c_uint32)]
         lib.rl_decode_attn_read_flags.restype = ctypes.c_int
         lib.rl_decode_attn_destroy.argtypes = [vp]

@@ -175,12 +175,23 @@ rlda_status rl_decode_attn_grouped_workspace_size(rl_decode_attn_t h, size_t* by
 
 namespace {
 
-// group_size == 0: plain run; > 0: grouped run with prefix_pages.
+// Device memory a plain run keeps its flags, counters and partials in, when it is
+// not the caller's workspace (the no-allocation entry point's static scratch).
+struct RunMem {
+  uint32_t* flags;
+  uint32_t* counters;
+  float* part_ml;
+  float* part_acc;
+  int ranges_cap;   // work ranges the partial slots are sized for
+};
+
+// group_size == 0: plain run; > 0: grouped run with prefix_pages.  With `mem` the
+// run uses it instead of a workspace (plain runs only).
 rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32_t group_size,
                      const int32_t* prefix_pages, int32_t prompt_pages_hint, const void* q, const void* k_cache, const void* v_cache,
                      const float* k_scale, const float* v_scale, const int32_t* block_table,
                      const int32_t* seq_lens, void* out, void* workspace, size_t workspace_bytes, void* stream,
-                     void* ev_begin, void* ev_end) {
+                     void* ev_begin, void* ev_end, const RunMem* mem = nullptr) {
   if (!h) return RLDA_ERR_INVALID_ARG;
   const rl_decode_attn_config& c = h->cfg;
   const bool grouped = group_size > 0;
@@ -197,8 +208,12 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32
   if (fp8 && num_pages > 0 && (!k_scale || !v_scale || ((uintptr_t)k_scale & 3u) || ((uintptr_t)v_scale & 3u)))
     return RLDA_ERR_INVALID_ARG;
   const WsLayout wl = layout_of(h);
-  if (!workspace || ((uintptr_t)workspace % kAlign)) return RLDA_ERR_WORKSPACE;
-  if (workspace_bytes < (grouped ? wl.grouped_total : wl.total)) return RLDA_ERR_WORKSPACE;
+  if (mem) {
+    if (grouped) return RLDA_ERR_UNSUPPORTED;
+  } else {
+    if (!workspace || ((uintptr_t)workspace % kAlign)) return RLDA_ERR_WORKSPACE;
+    if (workspace_bytes < (grouped ? wl.grouped_total : wl.total)) return RLDA_ERR_WORKSPACE;
+  }
 
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return RLDA_ERR_HIP;
@@ -209,7 +224,8 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32
     ranges = cu_count(dev);
     if (ranges <= 0) return RLDA_ERR_HIP;
   }
-  if (ranges > h->ws_ranges) ranges = h->ws_ranges;
+  const int ranges_cap = mem ? mem->ranges_cap : h->ws_ranges;
+  if (ranges > ranges_cap) ranges = ranges_cap;
   if (ranges > rlda::kMaxRanges) ranges = rlda::kMaxRanges;
   // Never more shares than (sequence, KV head, page) units could exist.
   const int64_t max_units = (int64_t)batch * c.num_kv_heads * c.max_pages_per_seq;
@@ -226,11 +242,11 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32
   p.block_table = block_table;
   p.seq_lens = seq_lens;
   p.out = out;
-  p.flags = (uint32_t*)(ws + wl.flags);
-  p.counters = (uint32_t*)(ws + wl.counters);
+  p.flags = mem ? mem->flags : (uint32_t*)(ws + wl.flags);
+  p.counters = mem ? mem->counters : (uint32_t*)(ws + wl.counters);
   p.call_tag = next_call_tag();
-  p.part_ml = (float*)(ws + wl.part_ml);
-  p.part_acc = (float*)(ws + wl.part_acc);
+  p.part_ml = mem ? mem->part_ml : (float*)(ws + wl.part_ml);
+  p.part_acc = mem ? mem->part_acc : (float*)(ws + wl.part_acc);
   p.part_rows = h->group;
   const int eb = elem_bytes(c.kv_dtype);
   p.stride_page = h->stride_page * eb;
@@ -325,6 +341,28 @@ rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t h, int32_t batch, int32
   if (!event_begin || !event_end) return RLDA_ERR_INVALID_ARG;
   return run_impl(h, batch, num_pages, 0, nullptr, -1, q, k_cache, v_cache, k_scale, v_scale, block_table, seq_lens,
                   out, workspace, workspace_bytes, stream, event_begin, event_end);
+}
+
+rlda_status rl_decode_attn_run_noalloc(rl_decode_attn_t h, int32_t batch, int32_t num_pages, const void* q,
+                                       const void* k_cache, const void* v_cache, const float* k_scale,
+                                       const float* v_scale, const int32_t* block_table, const int32_t* seq_lens,
+                                       void* out, uint32_t* flags, void* stream) {
+  if (!h) return RLDA_ERR_INVALID_ARG;
+  const rl_decode_attn_config& c = h->cfg;
+  if (batch < 0 || batch > c.max_batch || num_pages < 0) return RLDA_ERR_INVALID_ARG;
+  if ((uintptr_t)flags & 3u) return RLDA_ERR_INVALID_ARG;
+  // The static scratch holds counters for batch * Hkv segments and partial slots of
+  // 16 rows of at most 128 elements; checked before any HIP call.
+  if ((int64_t)batch * c.num_kv_heads > rlda::kScratchMaxSegments || c.head_dim > 128) return RLDA_ERR_SCRATCH;
+  if (batch == 0) return RLDA_OK;
+  void* base = nullptr;
+  if (rlda::noalloc_scratch(&base) != 0) return RLDA_ERR_HIP;
+  char* sc = (char*)base;
+  const RunMem mem = {flags ? flags : (uint32_t*)sc, (uint32_t*)(sc + rlda::kScratchCountersOff),
+                      (float*)(sc + rlda::kScratchMlOff), (float*)(sc + rlda::kScratchAccOff),
+                      rlda::kScratchMaxRanges};
+  return run_impl(h, batch, num_pages, 0, nullptr, -1, q, k_cache, v_cache, k_scale, v_scale, block_table, seq_lens,
+                  out, nullptr, 0, stream, nullptr, nullptr, &mem);
 }
 
 rlda_status rl_decode_attn_run_grouped(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32_t group_size,
@@ -509,6 +547,7 @@ const char* rl_decode_attn_strerror(rlda_status s) {
     case RLDA_ERR_HIP: return "HIP runtime error";
     case RLDA_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
     case RLDA_ERR_ALLOC: return "host allocation failed";
+    case RLDA_ERR_SCRATCH: return "request exceeds the static scratch of the no-allocation entry point";
   }
   return "unknown status";
 }

@@ -48,8 +48,17 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "rlda_device.h"
 #include "rlda_params.h"
+
+// Flags, segment counters and partial slots of rl_decode_attn_run_noalloc, for
+// callers that cannot allocate device memory (layout in rlda_params.h).  Each GPU
+// the library runs on holds its own copy until the process ends.  In host code the
+// name stands for a host-side handle, never a device address: the address comes
+// from hipGetSymbolAddress (noalloc_scratch below).
+static __device__ __align__(256) unsigned char scratch[rlda::kScratchBytes];
 
 namespace rlda {
 namespace {
@@ -1614,7 +1623,24 @@ int launch_prompt_then_decode(const Params& p, int ngroups, void* stream, void* 
   return launch<Mfma<D, FP8>>(p, stream, nullptr, ev_end);
 }
 
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64];
+
 }  // namespace
+
+int noalloc_scratch(void** ptr) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return -1;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    // With `dev` current: this device's copy of the array.
+    void* a = nullptr;
+    if (hipGetSymbolAddress(&a, HIP_SYMBOL(scratch)) != hipSuccess || !a) return -1;
+    g_scratch_ptr[dev] = a;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return 0;
+}
 
 #define RLDA_DISPATCH(FN, ...)                                                  \
   switch (kind) {                                                               \

@@ -1,5 +1,6 @@
 // Internal launch parameters shared by the host entry points and the kernels.
 #pragma once
+#include <stddef.h>
 #include <stdint.h>
 
 namespace rlda {
@@ -36,6 +37,18 @@ constexpr uint32_t kFlagStaleCounter = 8u;   // a segment counter held another c
 constexpr int kCounterCountBits = 13;
 constexpr int kCounterTagBits = 32 - kCounterCountBits;
 constexpr uint32_t kMaxCallTag = (1u << kCounterTagBits) - 2;   // all-ones is never a tag
+
+// Static scratch of rl_decode_attn_run_noalloc (one copy per GPU, in the kernel
+// source): the flag word, then segment counters for batch * Hkv <= kScratchMaxSegments,
+// then two partial slots of kMaxGroup rows per work range for up to
+// kScratchMaxRanges ranges at head_dim 128.
+constexpr int kScratchMaxRanges = 256;
+constexpr int kScratchMaxSegments = 65536;
+constexpr size_t kScratchCountersOff = 256;
+constexpr size_t kScratchMlOff = kScratchCountersOff + sizeof(uint32_t) * kScratchMaxSegments;
+constexpr size_t kScratchAccOff = kScratchMlOff + sizeof(float) * 2 * kScratchMaxRanges * kMaxGroup * 2;
+constexpr size_t kScratchBytes = kScratchAccOff + sizeof(float) * 2 * kScratchMaxRanges * kMaxGroup * 128;
+static_assert(kScratchMlOff % 256 == 0 && kScratchAccOff % 256 == 0, "scratch regions stay 256-byte aligned");
 
 struct Params {
   const void* q;               // [batch][Hq][D]
@@ -99,6 +112,9 @@ int launch_grouped(KvKind kind, int head_dim, int group, const Params& p, int ng
                    void* ev_begin, void* ev_end);
 // KV append: one wave per (sequence, KV head).
 int launch_append(KvKind kind, int head_dim, const Params& p, void* stream);
+// Device address of the static scratch on the current device (kScratchBytes bytes),
+// looked up once per device; 0 on success.
+int noalloc_scratch(void** ptr);
 // Multi-token queries (rlda_multi.hip): one workgroup per (128-row query block, KV head).
 int launch_multi(KvKind kind, int head_dim, const Params& p, int grid, void* stream, void* ev_begin, void* ev_end);
 // Multi-token queries with at most 16 * tiles rows per (sequence, KV head) segment

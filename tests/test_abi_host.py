@@ -285,3 +285,22 @@ def test_multi_rejects_bad_arguments_before_launch(lib):
     assert st == 0
     assert multi(handle=h32) == -2        # fp32 caches: no multi-token path
     lib.rl_decode_attn_destroy(h32)
+
+
+def test_noalloc_rejects_requests_beyond_its_static_scratch_before_any_hip_call(lib):
+    """rl_decode_attn_run_noalloc keeps counters for batch * Hkv <= 65536 segments in
+    its static scratch; larger batches get RLDA_ERR_SCRATCH (-6) with nothing
+    launched, and a misaligned flag word RLDA_ERR_INVALID_ARG."""
+    st, h = create(lib, cfg(num_q_heads=16, num_kv_heads=16, max_batch=8192, max_pages_per_seq=4))
+    assert st == 0
+    p = ctypes.c_void_p(4096)
+    try:
+        args = lambda B, flags: (h, B, 10, p, p, p, None, None, p, p, p, flags, None)
+        assert lib.rl_decode_attn_run_noalloc(*args(4097, None)) == -6     # 4097 * 16 > 65536
+        assert lib.rl_decode_attn_run_noalloc(*args(8192, None)) == -6
+        assert lib.rl_decode_attn_run_noalloc(*args(100, ctypes.c_void_p(4098))) == -1   # flags not 4-byte aligned
+        assert lib.rl_decode_attn_run_noalloc(*args(9000, None)) == -1     # beyond max_batch
+        assert lib.rl_decode_attn_run_noalloc(*args(0, None)) == 0         # empty batch: nothing to do
+        assert lib.rl_decode_attn_strerror(-6).startswith(b"request exceeds the static scratch")
+    finally:
+        lib.rl_decode_attn_destroy(h)
