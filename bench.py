@@ -127,6 +127,26 @@ def copy_reference(args, torch, dev):
           flush=True)
 
 
+def probe_bench(args, torch, dev, w):
+    """Every launch shape of the two read-ceiling probes: the streaming read of a
+    --probe-gib GiB buffer, and the gather of the workload's (K, V) page tiles in the
+    order the decode kernel streams them, over --sets rotated copies of the pools."""
+    from paper_2607_09207_amd import accounting as A
+    from paper_2607_09207_amd import inputs as I
+    from paper_2607_09207_amd import probe
+    sets = [I.to_torch(w, dev)]
+    for _ in range(args.sets - 1):
+        s = dict(sets[0])
+        s["k_cache"] = sets[0]["k_cache"].clone()
+        s["v_cache"] = sets[0]["v_cache"].clone()
+        sets.append(s)
+    sbest, sall = probe.stream_read(torch, dev, gib=args.probe_gib)
+    tile = w.page_size * w.head_dim * A.DTYPE_BYTES[w.kv_dtype]
+    gbest, gall = probe.tile_gather(torch, dev, [(s["k_cache"], s["v_cache"]) for s in sets], probe.tile_offsets(w), tile)
+    print(json.dumps({"mode": "probe", "workload": w.name, "tile_bytes": tile, "stream_bytes": int(args.probe_gib * 2**30),
+                      "stream": sall, "gather": gall, "stream_best": sbest, "gather_best": gbest}), flush=True)
+
+
 def append_bench(args, torch, dev, w, h, ws):
     """Time the per-step KV append: every sequence writes its last token's K/V rows
     (seq_lens[b] - 1) for every KV head; fp8 caches also maintain their page scales."""
@@ -314,11 +334,12 @@ def main():
     ap.add_argument("--sets", type=int, default=3, help="KV pool copies rotated across calls")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of CPU oracle work (0 = skip)")
     ap.add_argument("--ranges", type=int, default=0, help="force the number of work ranges (tuning)")
-    ap.add_argument("--mode", choices=["attention", "append", "multi", "copy"], default="attention",
+    ap.add_argument("--mode", choices=["attention", "append", "multi", "copy", "probe"], default="attention",
                     help="append: the per-step KV append (rl_decode_attn_append) on the workload's last tokens; "
                          "multi: multi-token (prefill chunk) attention on a multi-token workload "
                          "(prompt_prefill_grpo_bf16, chunked_prefill_gqa_bf16); "
-                         "copy: a plain device copy of --copy-mib MiB, the reference for HBM counter scaling")
+                         "copy: a plain device copy of --copy-mib MiB, the reference for HBM counter scaling; "
+                         "probe: every launch shape of the read-ceiling probes on the workload's page tiles")
     ap.add_argument("--copy-mib", type=int, default=256)
     ap.add_argument("--check", choices=["on", "off"], default="on",
                     help="compare every output with the fp64 oracle after timing (exit 1 on a miss)")
@@ -366,6 +387,8 @@ def main():
                         num_work_ranges=args.ranges)
     if args.mode == "append":
         return append_bench(args, torch, dev, w, h, h.workspace(dev))
+    if args.mode == "probe":
+        return probe_bench(args, torch, dev, w)
     if (args.mode == "multi") != (w.q_start is not None):
         raise SystemExit("--mode multi goes with the multi-token workloads: " + ", ".join(I.MULTI_WORKLOADS))
     if args.mode == "multi":

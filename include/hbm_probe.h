@@ -23,9 +23,9 @@ extern "C" {
 #endif
 
 /* Read `bytes` (a multiple of 16) of `buf` once with `blocks` workgroups of
- * `threads` threads (a multiple of 64, at most 1024), each lane keeping `unroll`
- * (1, 2, 4, 8 or 16) 16-byte non-temporal loads in flight.  `sink` holds at least
- * `blocks` 32-bit words; a word is written only if a lane's folded value equals an
+ * `threads` threads (a multiple of 64, at most 512), each lane keeping a ring of
+ * `unroll` (1, 2, 4, 8 or 16) 16-byte non-temporal loads in flight.  `sink` holds
+ * at least `blocks` 32-bit words; a word is written only if a lane's folded value equals an
  * internal sentinel. */
 int hbm_probe_stream_read(const void* buf, uint64_t bytes, uint32_t* sink, int blocks, int threads, int unroll,
                           void* stream);
@@ -34,8 +34,8 @@ int hbm_probe_stream_read(const void* buf, uint64_t bytes, uint32_t* sink, int b
  * 4096) bytes at byte offset tile_offsets[e] of `k_pool` and the same of `v_pool`.
  * Every offset must keep the tile inside both pools (not checked on the device).
  * The list is cut into equal contiguous shares, one per wave of the grid (`blocks`
- * workgroups of `threads` threads), and each wave keeps `depth` (1 to 4) pairs in
- * flight.  `sink` as for hbm_probe_stream_read. */
+ * workgroups of `threads` threads), and each wave keeps a ring of `depth` (1 to 4)
+ * pairs in flight.  `sink` as for hbm_probe_stream_read. */
 int hbm_probe_tile_gather(const void* k_pool, const void* v_pool, const int64_t* tile_offsets, int64_t ntiles,
                           int tile_bytes, uint32_t* sink, int blocks, int threads, int depth, void* stream);
 

@@ -110,16 +110,17 @@ rlda_status rl_decode_attn_workspace_size(rl_decode_attn_t handle, size_t* bytes
  *   block_table  [batch][max_pages_per_seq] int32  page ids in [0, num_pages)
  *   seq_lens     [batch] int32                     0 <= L <= max_pages_per_seq*16
  *   out          [batch][Hq][d]                    out_dtype
- *   workspace    >= rl_decode_attn_workspace_size bytes, 256-byte aligned; zero-fill it
- *                before its first use so that the contract-flag word (which accumulates;
- *                it is the workspace's first 32-bit word) starts clear.  It also holds partial results and per-segment counters.
- *                Each call tags the counters it counts in, and every call that
- *                completes returns them to zero; a counter holding another call's
- *                count (a workspace that was not zero-filled, or one that another call
- *                was using at the same time) is restarted by this call and raises flag
- *                bit 3.  Calls that may overlap in time need separate workspaces: two
- *                such calls on one workspace restart each other's counts, so their
- *                split rows may be left unwritten (bit 3 is raised).
+ *   workspace    >= rl_decode_attn_workspace_size bytes, 256-byte aligned, zero-filled
+ *                before its first use.  It holds per-segment counters that every run
+ *                returns to zero, partial results (each stored with a tag of the call
+ *                that wrote it), and the contract-flag word (its first 32-bit word,
+ *                which accumulates).  A counter that is not zero when a run begins (a
+ *                workspace that was not zero-filled, or another run using it at the
+ *                same time) raises flag bit 3: the run counts more pieces than the
+ *                segment has, or merges a partial it did not write.  The rows of the
+ *                affected segments are then unspecified, and the counters stay dirty
+ *                until the workspace is zero-filled again.  Calls that may overlap in
+ *                time need separate workspaces.
  * Pointers q, k_cache, v_cache and out must be 16-byte aligned; with num_pages == 0
  * (all sequences empty) the cache and scale pointers may be NULL.
  * Device-side contract violations (a page id outside the pool, a length beyond
@@ -155,9 +156,10 @@ rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t handle, int32_t batch, 
  *   - flags: NULL, or a caller-owned device uint32_t (4-byte aligned) that receives
  *     the contract bits of rl_decode_attn_read_flags (OR-ed in; the caller clears
  *     it).  With NULL they go to a word of the static array that nothing reads.
- * Nothing in the array needs clearing between calls (every call tags its segment
- * counters).  Every call on one GPU shares that GPU's array: calls that may
- * overlap in time (different streams) race on it and must not be issued.
+ * The array starts zeroed and every call that completes leaves its counters at
+ * zero, so nothing needs clearing between calls.  Every call on one GPU shares that
+ * GPU's array: calls that may overlap in time (different streams) race on it and
+ * must not be issued (flag bit 3 reports it when they meet).
  * No device memory is allocated or freed; one kernel, asynchronous.
  */
 rlda_status rl_decode_attn_run_noalloc(rl_decode_attn_t handle, int32_t batch, int32_t num_pages, const void* q,
@@ -293,8 +295,9 @@ rlda_status rl_decode_attn_run_multi(rl_decode_attn_t handle, int32_t batch, int
 /* Flags raised by device-side contract checks since the workspace was zeroed
  * (bit 0: page id outside [0, num_pages); bit 1: seq_len beyond capacity;
  * bit 2: a group's shared prompt clamped to its shortest member; bit 3: a
- * segment counter held another call's count when this call first counted in it:
- * the workspace was not zero-filled, or calls overlapped on it).
+ * segment counter was not zero when the run began, so the run counted more pieces
+ * than a segment has or merged a partial it had not written: the workspace was not
+ * zero-filled, or runs overlapped on it).
  * SYNCHRONISES `stream` (waits for queued work, copies 4 bytes to the host). */
 rlda_status rl_decode_attn_read_flags(rl_decode_attn_t handle, const void* workspace, void* stream,
                                       uint32_t* flags);

@@ -25,6 +25,12 @@ def _torch():
     return torch
 
 
+def _torch_dtype(code: int):
+    torch = _torch()
+    return {_abi.RLDA_F32: torch.float32, _abi.RLDA_BF16: torch.bfloat16,
+            _abi.RLDA_FP8_E4M3FN: torch.float8_e4m3fn}[code]
+
+
 def _dtype_code(t) -> int:
     torch = _torch()
     if t in (torch.float32, "f32"):
@@ -62,6 +68,9 @@ class DecodeAttention:
         if kv_strides is not None:
             cfg.kv_stride_page, cfg.kv_stride_head, cfg.kv_stride_slot = [int(x) for x in kv_strides]
         cfg.num_work_ranges = int(num_work_ranges)
+        P, d = page_size, head_dim
+        self._kv_strides = (tuple(int(x) for x in kv_strides) if kv_strides is not None
+                            else (num_kv_heads * P * d, P * d, d))
         h = ctypes.c_void_p()
         _abi.check(lib.rl_decode_attn_create(ctypes.byref(cfg), ctypes.byref(h)), "rl_decode_attn_create")
         self._lib, self._h, self.config = lib, h, cfg
@@ -91,6 +100,70 @@ class DecodeAttention:
             self._ws[key] = ws
         return ws
 
+    # ---------------------------------------------------------------- argument checks
+    # The kernels index the tensors by the handle's configuration; a tensor of the
+    # wrong device, dtype, shape or layout is rejected here, before any launch.
+
+    def _fail(self, what: str, msg: str):
+        raise RldaError(-1, f"{what}: {msg}")
+
+    def _tensor(self, what, name, t, dtype, shape, device, contiguous=True):
+        if t is None:
+            self._fail(what, f"{name} is required")
+        if not t.is_cuda or t.device != device:
+            self._fail(what, f"{name} must be on {device}, got {t.device}")
+        if t.dtype != dtype:
+            self._fail(what, f"{name} must be {dtype}, got {t.dtype}")
+        if tuple(t.shape) != tuple(shape):
+            self._fail(what, f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+        if contiguous and not t.is_contiguous():
+            self._fail(what, f"{name} must be contiguous")
+
+    def _check_cache(self, what, k_cache, v_cache, k_scale, v_scale, npages, device):
+        cfg = self.config
+        kvd = _torch_dtype(cfg.kv_dtype)
+        for name, t in (("k_cache", k_cache), ("v_cache", v_cache)):
+            if t is None:
+                self._fail(what, f"{name} is required")
+            if not t.is_cuda or t.device != device:
+                self._fail(what, f"{name} must be on {device}, got {t.device}")
+            if t.dtype != kvd:
+                self._fail(what, f"{name} must be {kvd}, got {t.dtype}")
+            if t.dim() != 4 or tuple(t.shape[1:]) != (cfg.num_kv_heads, cfg.page_size, cfg.head_dim):
+                self._fail(what, f"{name} must be [pages, {cfg.num_kv_heads}, {cfg.page_size}, {cfg.head_dim}], "
+                                 f"got {tuple(t.shape)}")
+            if tuple(t.stride()[:3]) != self._kv_strides or t.stride(3) != 1:
+                self._fail(what, f"{name} strides {tuple(t.stride())} differ from the handle's {self._kv_strides} "
+                                 "(head_dim contiguous)")
+            if t.shape[0] < npages:
+                self._fail(what, f"{name} holds {t.shape[0]} pages, fewer than num_pages = {npages}")
+        if cfg.kv_dtype == _abi.RLDA_FP8_E4M3FN:
+            torch = _torch()
+            for name, t in (("k_scale", k_scale), ("v_scale", v_scale)):
+                if t is None:
+                    self._fail(what, f"{name} is required for fp8 caches")
+                if t.dim() != 2 or t.shape[1] != cfg.num_kv_heads or t.shape[0] < npages:
+                    self._fail(what, f"{name} must be [>= {npages}, {cfg.num_kv_heads}], got {tuple(t.shape)}")
+                self._tensor(what, name, t, torch.float32, tuple(t.shape), device)
+
+    def _check_rows(self, what, q, out, rows, device):
+        cfg = self.config
+        shape = (rows, cfg.num_q_heads, cfg.head_dim)
+        self._tensor(what, "q", q, _torch_dtype(cfg.q_dtype), shape, device)
+        self._tensor(what, "out", out, _torch_dtype(cfg.out_dtype), shape, device)
+
+    def _check_table(self, what, block_table, seq_lens, batch, device):
+        torch = _torch()
+        if batch > self.config.max_batch:
+            self._fail(what, f"batch {batch} exceeds max_batch {self.config.max_batch}")
+        self._tensor(what, "block_table", block_table, torch.int32, (batch, self.config.max_pages_per_seq), device)
+        self._tensor(what, "seq_lens", seq_lens, torch.int32, (batch,), device)
+
+    def _check_workspace(self, what, ws, device):
+        torch = _torch()
+        if not ws.is_cuda or ws.device != device or ws.dtype != torch.uint8 or not ws.is_contiguous():
+            self._fail(what, f"workspace must be a contiguous uint8 tensor on {device}")
+
     @staticmethod
     def _aligned_ptr(ws) -> int:
         p = ws.data_ptr()
@@ -116,16 +189,28 @@ class DecodeAttention:
         torch = _torch()
         B = int(q.shape[0])
         cfg = self.config
+        what = "rl_decode_attn_run_grouped" if group_size is not None else "rl_decode_attn_run"
+        if not q.is_cuda:
+            self._fail(what, f"q must be on a GPU, got {q.device}")
         if out is None:
             odt = torch.float32 if cfg.out_dtype == _abi.RLDA_F32 else torch.bfloat16
             out = torch.empty((B, cfg.num_q_heads, cfg.head_dim), dtype=odt, device=q.device)
+        npages = int(k_cache.shape[0]) if num_pages is None else int(num_pages)
+        self._check_rows(what, q, out, B, q.device)
+        self._check_table(what, block_table, seq_lens, B, q.device)
+        self._check_cache(what, k_cache, v_cache, k_scale, v_scale, npages, q.device)
         grouped = group_size is not None
+        if grouped:
+            if int(group_size) < 1:
+                self._fail(what, "group_size must be >= 1")
+            ng = (B + int(group_size) - 1) // int(group_size)
+            self._tensor(what, "prefix_pages", prefix_pages, torch.int32, (ng,), q.device)
         ws = workspace if workspace is not None else self.workspace(q.device, grouped=grouped)
+        self._check_workspace(what, ws, q.device)
         if stream is None:
             stream = torch.cuda.current_stream(q.device).cuda_stream
         elif hasattr(stream, "cuda_stream"):
             stream = stream.cuda_stream
-        npages = int(k_cache.shape[0]) if num_pages is None else int(num_pages)
         ptr = lambda t: None if t is None else t.data_ptr()
         wp = self._aligned_ptr(ws)
         args = (self._h, B, npages, ptr(q), ptr(k_cache), ptr(v_cache), ptr(k_scale), ptr(v_scale),
@@ -150,14 +235,22 @@ class DecodeAttention:
         torch = _torch()
         B = int(q.shape[0])
         cfg = self.config
+        what = "rl_decode_attn_run_noalloc"
+        if not q.is_cuda:
+            self._fail(what, f"q must be on a GPU, got {q.device}")
         if out is None:
             odt = torch.float32 if cfg.out_dtype == _abi.RLDA_F32 else torch.bfloat16
             out = torch.empty((B, cfg.num_q_heads, cfg.head_dim), dtype=odt, device=q.device)
+        npages = int(k_cache.shape[0]) if num_pages is None else int(num_pages)
+        self._check_rows(what, q, out, B, q.device)
+        self._check_table(what, block_table, seq_lens, B, q.device)
+        self._check_cache(what, k_cache, v_cache, k_scale, v_scale, npages, q.device)
+        if flags is not None:
+            self._tensor(what, "flags", flags, torch.int32, (1,), q.device)
         if stream is None:
             stream = torch.cuda.current_stream(q.device).cuda_stream
         elif hasattr(stream, "cuda_stream"):
             stream = stream.cuda_stream
-        npages = int(k_cache.shape[0]) if num_pages is None else int(num_pages)
         ptr = lambda t: None if t is None else t.data_ptr()
         _abi.check(self._lib.rl_decode_attn_run_noalloc(self._h, B, npages, ptr(q), ptr(k_cache), ptr(v_cache),
                                                         ptr(k_scale), ptr(v_scale), ptr(block_table), ptr(seq_lens),
@@ -176,15 +269,23 @@ class DecodeAttention:
         total = int(q.shape[0])
         B = int(q_start.shape[0]) - 1
         cfg = self.config
+        what = "rl_decode_attn_run_multi"
+        if not q.is_cuda:
+            self._fail(what, f"q must be on a GPU, got {q.device}")
         if out is None:
             odt = torch.float32 if cfg.out_dtype == _abi.RLDA_F32 else torch.bfloat16
             out = torch.empty((total, cfg.num_q_heads, cfg.head_dim), dtype=odt, device=q.device)
+        npages = int(k_cache.shape[0]) if num_pages is None else int(num_pages)
+        self._check_rows(what, q, out, total, q.device)
+        self._tensor(what, "q_start", q_start, torch.int32, (B + 1,), q.device)
+        self._check_table(what, block_table, seq_lens, B, q.device)
+        self._check_cache(what, k_cache, v_cache, k_scale, v_scale, npages, q.device)
         ws = workspace if workspace is not None else self.workspace(q.device)
+        self._check_workspace(what, ws, q.device)
         if stream is None:
             stream = torch.cuda.current_stream(q.device).cuda_stream
         elif hasattr(stream, "cuda_stream"):
             stream = stream.cuda_stream
-        npages = int(k_cache.shape[0]) if num_pages is None else int(num_pages)
         ptr = lambda t: None if t is None else t.data_ptr()
         wp = self._aligned_ptr(ws)
         e0, e1 = (None, None) if events is None else tuple(self._event_handle(e) for e in events)
@@ -203,12 +304,22 @@ class DecodeAttention:
         update their per-page scales."""
         torch = _torch()
         B = int(k_new.shape[0])
-        ws = workspace if workspace is not None else self.workspace(k_new.device)
+        cfg = self.config
+        what = "rl_decode_attn_append"
+        if not k_new.is_cuda:
+            self._fail(what, f"k_new must be on a GPU, got {k_new.device}")
+        dev = k_new.device
+        npages = int(k_cache.shape[0]) if num_pages is None else int(num_pages)
+        for name, t in (("k_new", k_new), ("v_new", v_new)):
+            self._tensor(what, name, t, _torch_dtype(cfg.q_dtype), (B, cfg.num_kv_heads, cfg.head_dim), dev)
+        self._check_table(what, block_table, seq_lens, B, dev)
+        self._check_cache(what, k_cache, v_cache, k_scale, v_scale, npages, dev)
+        ws = workspace if workspace is not None else self.workspace(dev)
+        self._check_workspace(what, ws, dev)
         if stream is None:
-            stream = torch.cuda.current_stream(k_new.device).cuda_stream
+            stream = torch.cuda.current_stream(dev).cuda_stream
         elif hasattr(stream, "cuda_stream"):
             stream = stream.cuda_stream
-        npages = int(k_cache.shape[0]) if num_pages is None else int(num_pages)
         ptr = lambda t: None if t is None else t.data_ptr()
         wp = self._aligned_ptr(ws)
         _abi.check(self._lib.rl_decode_attn_append(self._h, B, npages, ptr(k_new), ptr(v_new), ptr(k_cache),

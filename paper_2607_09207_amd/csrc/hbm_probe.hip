@@ -3,13 +3,14 @@
 // the bench loads this library next to the attention library and reports the best
 // rate each kernel reaches over a few launch shapes.
 //
-//   stream read  - a contiguous buffer read once, 16 bytes per lane per load,
-//                  U loads in flight per lane, non-temporal (the data is not reused);
+//   stream read  - a contiguous buffer read once, 16 bytes per lane per load, a
+//                  ring of U loads in flight per lane, non-temporal (the data is
+//                  not reused);
 //   tile gather  - the decode kernel's access pattern without its arithmetic: a list
 //                  of (K, V) tile pairs at byte offsets into two pools (one pair per
 //                  (sequence, KV head, page) of a workload, in the order the decode
 //                  kernel streams them), cut into equal contiguous shares, one per
-//                  wave, with U tile pairs in flight per wave.
+//                  wave, with a ring of U tile pairs in flight per wave.
 // Both fold every loaded word into a per-lane value and store it only when it
 // equals a sentinel, so the loads cannot be removed and almost nothing is written.
 #include <hip/hip_runtime.h>
@@ -24,29 +25,45 @@ constexpr uint32_t kSentinel = 0x9E3779B9u;
 
 __device__ __forceinline__ uint32_t fold(u32x4 v) { return v[0] ^ v[1] ^ v[2] ^ v[3]; }
 
+// Thread t of the grid reads elements t, t + N, t + 2N, ... (N threads) as a ring
+// of U loads: the load U - 1 elements ahead is issued before each element is
+// folded, so U loads stay in flight from the first element to the last.
 template <int U>
-__global__ void stream_read_kernel(const u32x4* __restrict__ buf, uint64_t n16, uint32_t* __restrict__ sink) {
-  const uint64_t nthreads = (uint64_t)gridDim.x * blockDim.x;
-  uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+__global__ __attribute__((amdgpu_flat_work_group_size(64, 512))) void stream_read_kernel(const u32x4* __restrict__ buf, uint64_t n16, uint32_t* __restrict__ sink) {
+  const uint64_t N = (uint64_t)gridDim.x * blockDim.x;
+  const uint64_t i0 = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const uint64_t cnt = i0 < n16 ? (n16 - i0 + N - 1) / N : 0;   // elements of this thread
+  const u32x4* p = buf + i0;
+  u32x4 r[U];
   uint32_t acc = 0;
-  // Full rounds: U loads per lane, all addresses in range.
-  for (; i + (U - 1) * nthreads < n16; i += U * nthreads) {
-    u32x4 v[U];
 #pragma unroll
-    for (int k = 0; k < U; ++k) v[k] = __builtin_nontemporal_load(buf + i + k * nthreads);
+  for (int k = 0; k < U - 1; ++k)
+    if ((uint64_t)k < cnt) r[k] = __builtin_nontemporal_load(p + k * N);
+  uint64_t j = 0;
+  for (; j + 2 * U - 2 < cnt; j += U) {   // every index issued here is below cnt
 #pragma unroll
-    for (int k = 0; k < U; ++k) acc ^= fold(v[k]);
+    for (int k = 0; k < U; ++k) {
+      r[(k + U - 1) % U] = __builtin_nontemporal_load(p + (j + k + U - 1) * N);
+      acc ^= fold(r[k]);
+    }
   }
-  for (; i < n16; i += nthreads) acc ^= fold(__builtin_nontemporal_load(buf + i));
+  for (; j < cnt; j += U) {
+#pragma unroll
+    for (int k = 0; k < U; ++k) {
+      if (j + k + U - 1 < cnt) r[(k + U - 1) % U] = __builtin_nontemporal_load(p + (j + k + U - 1) * N);
+      if (j + k < cnt) acc ^= fold(r[k]);
+    }
+  }
   if (acc == kSentinel) sink[blockIdx.x] = acc;
 }
 
 // Wave w of the grid reads entries [w*n/W, (w+1)*n/W) of the offset list: for each,
-// the K tile and the V tile of `tile_bytes` at that byte offset.  Lane l loads bytes
-// [16 l, 16 l + 16) of each 1 KiB quarter-row group, so one load instruction of the
-// wave covers 1 KiB contiguous.
+// the K tile and the V tile of `tile_bytes` at that byte offset, lane l loading bytes
+// [16 l, 16 l + 16) of every 1 KiB of the tile (one load instruction of the wave
+// covers 1 KiB contiguous).  The entries go through a ring of U: the tiles of entry
+// e + U - 1 are issued before entry e is folded.
 template <int U>
-__global__ void tile_gather_kernel(const char* __restrict__ k, const char* __restrict__ v,
+__global__ __attribute__((amdgpu_flat_work_group_size(64, 512))) void tile_gather_kernel(const char* __restrict__ k, const char* __restrict__ v,
                                    const int64_t* __restrict__ off, int64_t n, int tile_bytes,
                                    uint32_t* __restrict__ sink) {
   const int lane = threadIdx.x & 63;
@@ -55,24 +72,37 @@ __global__ void tile_gather_kernel(const char* __restrict__ k, const char* __res
   const int64_t e0 = w * n / waves, e1 = (w + 1) * n / waves;
   const int per = tile_bytes / 1024;   // 1 KiB load instructions per tile
   uint32_t acc = 0;
-  for (int64_t e = e0; e < e1; e += U) {
-    u32x4 kv[U][2][4];
+  u32x4 kv[U][2][4];
+  auto issue = [&](u32x4 (&t)[2][4], int64_t e) {
+    const int64_t o = off[e];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int64_t b = o + (int64_t)c * 1024 + lane * 16;
+      t[0][c] = c < per ? __builtin_nontemporal_load((const u32x4*)(k + b)) : u32x4{0, 0, 0, 0};
+      t[1][c] = c < per ? __builtin_nontemporal_load((const u32x4*)(v + b)) : u32x4{0, 0, 0, 0};
+    }
+  };
+  auto consume = [&](const u32x4 (&t)[2][4]) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc ^= fold(t[0][c]) ^ fold(t[1][c]);
+  };
+#pragma unroll
+  for (int u = 0; u < U - 1; ++u)
+    if (e0 + u < e1) issue(kv[u], e0 + u);
+  int64_t e = e0;
+  for (; e + 2 * U - 2 < e1; e += U) {   // every entry issued here is below e1
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const bool ok = e + u < e1;
-      const int64_t o = ok ? off[e + u] : off[e0];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int64_t b = o + (int64_t)c * 1024 + lane * 16;
-        const bool in = ok && c < per;
-        kv[u][0][c] = in ? __builtin_nontemporal_load((const u32x4*)(k + b)) : u32x4{0, 0, 0, 0};
-        kv[u][1][c] = in ? __builtin_nontemporal_load((const u32x4*)(v + b)) : u32x4{0, 0, 0, 0};
-      }
+      issue(kv[(u + U - 1) % U], e + u + U - 1);
+      consume(kv[u]);
     }
+  }
+  for (; e < e1; e += U) {
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int c = 0; c < 4; ++c) acc ^= fold(kv[u][0][c]) ^ fold(kv[u][1][c]);
+    for (int u = 0; u < U; ++u) {
+      if (e + u + U - 1 < e1) issue(kv[(u + U - 1) % U], e + u + U - 1);
+      if (e + u < e1) consume(kv[u]);
+    }
   }
   if (acc == kSentinel) sink[blockIdx.x] = acc;
 }
@@ -92,7 +122,8 @@ int launch_gather(const void* k, const void* v, const int64_t* off, int64_t n, i
 }
 
 bool shape_ok(int blocks, int threads) {
-  return blocks >= 1 && blocks <= (1 << 20) && threads >= 64 && threads <= 1024 && threads % 64 == 0;
+  // at most 512 threads: each wave may then use up to 256 registers (the rings)
+  return blocks >= 1 && blocks <= (1 << 20) && threads >= 64 && threads <= 512 && threads % 64 == 0;
 }
 
 }  // namespace

@@ -49,7 +49,7 @@ WsLayout layout_of(const rlda_handle* h) {
   w.part_ml = align_up(w.counters + sizeof(uint32_t) * (size_t)c.max_batch * c.num_kv_heads * rlda::kMaxRowChunks);
   // Partial slots: two per work range, 16 rows each (G rows in decode runs, up to
   // 16 rows of a segment in multi-token runs).
-  w.part_acc = align_up(w.part_ml + sizeof(float) * 2 * (size_t)h->ws_ranges * rlda::kMaxGroup * 2);
+  w.part_acc = align_up(w.part_ml + sizeof(float) * 4 * (size_t)h->ws_ranges * rlda::kMaxGroup * 2);
   w.total = align_up(w.part_acc + sizeof(float) * 2 * (size_t)h->ws_ranges * rlda::kMaxGroup * c.head_dim);
   w.gprefix = w.total;
   w.pfx_ml = align_up(w.gprefix + sizeof(int32_t) * (size_t)c.max_batch);
@@ -75,12 +75,18 @@ int cu_count(int dev) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-// Counter tags: one per call, cycling over [1, kMaxCallTag] across the process, so
-// a segment counter left by a call that did not complete (or never zeroed) is
-// told apart from this call's count.
+// Call tags: published with every partial so that a merge can tell a piece of this
+// call from a stale one.  Consecutive calls get well-spread values (a multiplicative
+// hash of a process-wide sequence number); 0 and all-ones, what zeroed or
+// never-written memory holds, are skipped.
 std::atomic<uint32_t> g_call_seq{0};
 
-uint32_t next_call_tag() { return g_call_seq.fetch_add(1, std::memory_order_relaxed) % rlda::kMaxCallTag + 1; }
+uint32_t next_call_tag() {
+  for (;;) {
+    const uint32_t t = (g_call_seq.fetch_add(1, std::memory_order_relaxed) * 2654435761u) ^ 0xA5A5A5A5u;
+    if (t != 0u && t != 0xFFFFFFFFu) return t;
+  }
+}
 
 }  // namespace
 

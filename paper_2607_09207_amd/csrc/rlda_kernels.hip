@@ -31,13 +31,14 @@
 //      wave.  The cut pieces (at most 2 per wave) are merged through LDS.  A piece
 //      of a segment that is split across workgroups stores its unnormalised
 //      partial with device-scope (sc1) stores, which write through the XCD's L2;
-//      after they complete, the workgroup bumps the segment's counter (tagged
-//      with the call, so a counter another call left behind is detected and
-//      restarted).  The workgroup that completes the count reads every piece of
-//      the segment with device-scope loads, merges them in piece order with
-//      log-sum-exp weights, writes the output and resets the counter.  No
-//      workgroup waits for another, and no device-scope fence (a whole-L2
-//      writeback and invalidate per XCD) is issued.
+//      after they complete, the workgroup bumps the segment's counter.  The
+//      workgroup that completes the count reads every piece of the segment with
+//      device-scope loads, merges them in piece order with log-sum-exp weights,
+//      writes the output and resets the counter.  Each partial carries the
+//      call's tag, so a merge that meets a piece this call did not publish (a
+//      counter left non-zero in the workspace) raises a flag.  No workgroup waits
+//      for another, and no device-scope fence (a whole-L2 writeback and
+//      invalidate per XCD) is issued.
 // fp8 (OCP E4M3FN) caches are converted exactly to bf16 for the MFMA; the K
 // scale multiplies the scores and the V scale multiplies P.  fp32 caches use a
 // VALU path.
@@ -145,7 +146,7 @@ __device__ __forceinline__ void store_out(const Params& p, int b, int qh, int d0
 __shared__ int16_t s_qhead[kMaxQHeads];
 
 // Partials of split segments live in the workspace: slot sl of query row h holds
-// (m, l) at part_ml[(sl*R + h)*2] and the unnormalised output at
+// (m, l, call tag, 0) at part_ml[(sl*R + h)*4] and the unnormalised output at
 // part_acc[(sl*R + h)*D ...], sl < 2*nranges, R = part_rows (G, or the rows of a
 // multi-token segment).  They are written and read with the
 // sc1 cache policy (device scope: write-through past the XCD's L2 and read from
@@ -157,34 +158,9 @@ struct PartialRsrc {
   template <int D>
   __device__ __forceinline__ static PartialRsrc of(const Params& p) {
     const uint32_t slots = 2u * (uint32_t)p.nranges * (uint32_t)p.part_rows;
-    return {make_rsrc_uni(p.part_acc, slots * D * 4u), make_rsrc_uni(p.part_ml, slots * 8u)};
+    return {make_rsrc_uni(p.part_acc, slots * D * 4u), make_rsrc_uni(p.part_ml, slots * 16u)};
   }
 };
-
-static_assert(kMaxRanges < (1 << kCounterCountBits), "piece counts must fit the counter's count field");
-
-// Count one finished piece of a split segment in its counter word; returns the
-// pieces of this call counted so far, this one included.  A word holding another
-// call's tag with a nonzero count was left by a call that never completed on this
-// workspace, or the workspace was not zero-filled: the count restarts from this
-// piece (so the result is unaffected) and kFlagStaleCounter is raised.  Lock-free:
-// a failed compare-and-swap means another piece's succeeded.
-__device__ __forceinline__ uint32_t count_piece(uint32_t* ctr, uint32_t tag, uint32_t* flags) {
-  constexpr uint32_t kMask = (1u << kCounterCountBits) - 1;
-  uint32_t old = __hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  uint32_t nw;
-  bool stale;
-  for (;;) {
-    const bool mine = (old >> kCounterCountBits) == tag;
-    stale = !mine && old != 0;
-    nw = mine ? old + 1 : (tag << kCounterCountBits) | 1u;
-    const uint32_t prev = atomicCAS(ctr, old, nw);
-    if (prev == old) break;
-    old = prev;
-  }
-  if (stale) atomicOr(flags, kFlagStaleCounter);
-  return nw & kMask;
-}
 
 // Online log-sum-exp merge of one partial (mj, lj, v[]) into (M, Ls, o[]).
 template <int N>
@@ -206,14 +182,15 @@ template <int D, int kBatch, int DPT>
 __device__ __forceinline__ void merge_batches(const Params& p, const PartialRsrc& rs, int h, int d0, int64_t u_first,
                                               int64_t u_last, float& M, float& Ls, float* o) {
   const int G = p.part_rows;
+  bool stale = false;
   for (int64_t k0 = u_first; k0 <= u_last; k0 += kBatch) {
-    u32x2 ml[kBatch];
+    u32x4 ml[kBatch];
     float v[kBatch][DPT];
 #pragma unroll
     for (int i = 0; i < kBatch; ++i) {
       const int64_t k = min(k0 + i, u_last);   // past the last piece: re-read it, unused
       const int sl = (int)((k < u_last) ? 2 * k + 1 : 2 * k);
-      ml[i] = __builtin_amdgcn_raw_buffer_load_b64(rs.ml, (sl * G + h) * 8, 0, kDeviceScope);
+      ml[i] = __builtin_amdgcn_raw_buffer_load_b128(rs.ml, (sl * G + h) * 16, 0, kDeviceScope);
 #pragma unroll
       for (int c = 0; c < DPT; c += 4)
         *(u32x4*)&v[i][c] = __builtin_amdgcn_raw_buffer_load_b128(rs.acc, ((sl * G + h) * D + d0 + c) * 4, 0,
@@ -221,9 +198,14 @@ __device__ __forceinline__ void merge_batches(const Params& p, const PartialRsrc
     }
 #pragma unroll
     for (int i = 0; i < kBatch; ++i)
-      if (k0 + i <= u_last)
+      if (k0 + i <= u_last) {
+        stale |= ml[i][2] != p.call_tag;
         lse_merge<DPT>(M, Ls, o, __uint_as_float(ml[i][0]), __uint_as_float(ml[i][1]), v[i]);
+      }
   }
+  // A piece this call has not published: the segment's counter was not zero when the
+  // call began (a workspace that was not zero-filled, or calls overlapping on it).
+  if (__builtin_amdgcn_ballot_w64(stale) != 0 && (threadIdx.x & 63) == 0) atomicOr(p.flags, kFlagStaleState);
 }
 
 // A segment cut into many pieces (a long sequence over few workgroups' worth of
@@ -852,7 +834,10 @@ void decode_attention_kernel(const Params p) {
   const int nunits = PACK ? p.pack_units : batch;
   if constexpr (PACK) {
     // Pages and last-page tokens of every sequence, then each group's prompt pages:
-    // the requested count clamped to the full pages of its shortest member.
+    // the requested count clamped to the full pages of its shortest member.  The
+    // first requested counts are loaded together with the lengths.
+    const int gs = p.group_size, ngroups = (batch + gs - 1) / gs;
+    const int want0 = tid < ngroups ? p.prefix_pages[tid] : 0;
     int bad = 0;
     for (int b = tid; b < batch; b += kThreads) {
       int L = p.seq_lens[b];
@@ -864,14 +849,13 @@ void decode_attention_kernel(const Params p) {
     }
     if (bad && u == 0) atomicOr(p.flags, kFlagBadLen);
     __syncthreads();
-    const int gs = p.group_size, ngroups = (batch + gs - 1) / gs;
     for (int i = tid; i < ngroups; i += kThreads) {
       int mn = 0x7fffffff;
       for (int b = i * gs; b < min(batch, (i + 1) * gs); ++b) {
         const int nf = s_nfull[b];
         mn = min(mn, (nf > 0 && s_tail[b] < kPage) ? nf - 1 : nf);   // full pages
       }
-      const int want = p.prefix_pages[i], pp = max(0, min(want, mn));
+      const int want = i == tid ? want0 : p.prefix_pages[i], pp = max(0, min(want, mn));
       if (want != pp && u == 0) atomicOr(p.flags, kFlagPrefixClamped);
       s_gpp[i] = (int16_t)pp;
     }
@@ -1252,9 +1236,9 @@ void decode_attention_kernel(const Params p) {
           for (int c = 0; c < DPT; c += 4)
             __builtin_amdgcn_raw_buffer_store_b128(*(const u32x4*)&o[c], rs.acc, ((gs * R + hr) * D + d0 + c) * 4, 0,
                                                    kDeviceScope);
-          if (tid % kTPR == 0)   // one thread per row stores its (m, l)
-            __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(M), __float_as_uint(Ls)}, rs.ml,
-                                                  (gs * R + hr) * 8, 0, kDeviceScope);
+          if (tid % kTPR == 0)   // one thread per row stores its (m, l) and the call's tag
+            __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(M), __float_as_uint(Ls), p.call_tag, 0u},
+                                                   rs.ml, (gs * R + hr) * 16, 0, kDeviceScope);
         }
       }
       if (!whole && nhand < 2) hand_seg[nhand++] = cur;   // only the first and last group can be cut
@@ -1298,9 +1282,9 @@ void decode_attention_kernel(const Params p) {
     const int64_t seg_start = (int64_t)Hs * pre_b + (int64_t)g * nb;
     const uint32_t npieces = (uint32_t)(owner_of(cost_of(seg_start + nb - 1, b, g), Wn, C) -
                                         owner_of(cost_of(seg_start, b, g), Wn, C) + 1);
-    const uint32_t got = count_piece(p.counters + sgi, p.call_tag, p.flags);
-    if (got > npieces) atomicOr(p.flags, kFlagStaleCounter);   // more pieces than the segment has
-    s_last[tid] = (got == npieces);
+    const uint32_t old = atomicAdd(p.counters + sgi, 1u);
+    if (old >= npieces) atomicOr(p.flags, kFlagStaleState);   // more pieces than the segment has
+    s_last[tid] = (old + 1u == npieces);
   }
   __syncthreads();
   for (int i = 0; i < nhand; ++i) {
@@ -1465,7 +1449,11 @@ void prompt_kernel(const Params p) {
                                             kDeviceScope);
     __builtin_amdgcn_s_waitcnt(0);   // this wave's device-scope stores have completed
     __syncthreads();                 // ... and every other wave's
-    if (tid == 0) s_min = (count_piece(p.counters + job, p.call_tag, p.flags) == (uint32_t)S);
+    if (tid == 0) {
+      const uint32_t old = atomicAdd(p.counters + job, 1u);
+      if (old >= (uint32_t)S) atomicOr(p.flags, kFlagStaleState);   // more pieces than the job has
+      s_min = (old + 1u == (uint32_t)S);
+    }
     __syncthreads();
     if (!s_min) return;
     if (tid == 0) atomicExch(p.counters + job, 0u);

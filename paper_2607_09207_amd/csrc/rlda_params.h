@@ -28,15 +28,7 @@ constexpr int kMaxRowsQLen = 16;   // ... and at most 16 rows per sequence (a fu
 constexpr uint32_t kFlagBadPage = 1u;
 constexpr uint32_t kFlagBadLen = 2u;
 constexpr uint32_t kFlagPrefixClamped = 4u;
-constexpr uint32_t kFlagStaleCounter = 8u;   // a segment counter held another call's count
-
-// Segment counters: the high kCounterTagBits bits of a counter word hold the tag of
-// the call counting in it, the low bits the pieces counted so far (at most
-// kMaxRanges).  A word that is 0, or carries another call's tag, starts a fresh
-// count; 0 is what every merge leaves behind.  Tags run over [1, kMaxCallTag].
-constexpr int kCounterCountBits = 13;
-constexpr int kCounterTagBits = 32 - kCounterCountBits;
-constexpr uint32_t kMaxCallTag = (1u << kCounterTagBits) - 2;   // all-ones is never a tag
+constexpr uint32_t kFlagStaleState = 8u;   // a counter or a partial this call did not write (workspace not zeroed)
 
 // Static scratch of rl_decode_attn_run_noalloc (one copy per GPU, in the kernel
 // source): the flag word, then segment counters for batch * Hkv <= kScratchMaxSegments,
@@ -46,7 +38,7 @@ constexpr int kScratchMaxRanges = 256;
 constexpr int kScratchMaxSegments = 65536;
 constexpr size_t kScratchCountersOff = 256;
 constexpr size_t kScratchMlOff = kScratchCountersOff + sizeof(uint32_t) * kScratchMaxSegments;
-constexpr size_t kScratchAccOff = kScratchMlOff + sizeof(float) * 2 * kScratchMaxRanges * kMaxGroup * 2;
+constexpr size_t kScratchAccOff = kScratchMlOff + sizeof(float) * 4 * kScratchMaxRanges * kMaxGroup * 2;
 constexpr size_t kScratchBytes = kScratchAccOff + sizeof(float) * 2 * kScratchMaxRanges * kMaxGroup * 128;
 static_assert(kScratchMlOff % 256 == 0 && kScratchAccOff % 256 == 0, "scratch regions stay 256-byte aligned");
 
@@ -60,10 +52,10 @@ struct Params {
   const int32_t* seq_lens;     // [batch]
   void* out;                   // [batch][Hq][D]
   float* part_acc;             // [2 * nranges][part_rows][D]  unnormalised partial outputs
-  float* part_ml;              // [2 * nranges][part_rows][2]  (running max in log2 units, sum)
+  float* part_ml;              // [2 * nranges][part_rows][4]  (running max in log2 units, sum, call tag, 0)
   int32_t part_rows;           // query rows per (sequence, KV head) segment: G, or n_max * G for multi-token rows
-  uint32_t* counters;          // [max_batch * Hkv * 4] (call tag, finished pieces) per split segment
-  uint32_t call_tag;           // this call's counter tag, in [1, kMaxCallTag]
+  uint32_t* counters;          // [max_batch * Hkv * 4] finished pieces per split segment; zero between runs
+  uint32_t call_tag;           // this call's tag, published with each partial (never 0 or all-ones)
   uint32_t* flags;             // contract-violation bits
   int64_t stride_page;         // bytes
   int64_t stride_head;         // bytes

@@ -55,7 +55,7 @@ def stream_read(torch, dev, gib: float = 4.0, reps: int = 10, cus: int = 256):
     stream = torch.cuda.current_stream(dev)
     sink = torch.zeros(cus * 64, dtype=torch.int32, device=dev)
     res = []
-    for per_cu, threads in ((1, 256), (2, 256), (4, 256), (2, 512), (8, 256)):
+    for per_cu, threads in ((1, 256), (2, 256), (4, 256), (1, 512), (2, 512)):
         for unroll in (4, 8, 16):
             blocks = per_cu * cus
 

@@ -50,6 +50,7 @@ def test_probe_library_exports_its_declared_functions():
     assert plib.hbm_probe_stream_read(None, 1024, sink, 1, 256, 8, None) == -1          # null buffer
     assert plib.hbm_probe_stream_read(ctypes.c_void_p(256), 1000, sink, 1, 256, 8, None) == -1   # not a multiple of 16
     assert plib.hbm_probe_stream_read(ctypes.c_void_p(256), 1024, sink, 1, 100, 8, None) == -1   # threads % 64
+    assert plib.hbm_probe_stream_read(ctypes.c_void_p(256), 1024, sink, 1, 1024, 8, None) == -1  # more than 512 threads
     assert plib.hbm_probe_stream_read(ctypes.c_void_p(256), 1024, sink, 1, 256, 3, None) == -1   # unroll
     assert plib.hbm_probe_tile_gather(ctypes.c_void_p(256), ctypes.c_void_p(256), None, 4, 4096, sink, 1, 256, 2,
                                       None) == -1                                              # no offsets
@@ -304,3 +305,20 @@ def test_noalloc_rejects_requests_beyond_its_static_scratch_before_any_hip_call(
         assert lib.rl_decode_attn_strerror(-6).startswith(b"request exceeds the static scratch")
     finally:
         lib.rl_decode_attn_destroy(h)
+
+
+def test_binding_rejects_host_tensors_before_any_launch(lib):
+    import torch
+    from paper_2607_09207_amd import DecodeAttention, RldaError
+    h = DecodeAttention(8, 2, 128, 4, 8)
+    q = torch.zeros((3, 8, 128), dtype=torch.bfloat16)
+    kv = torch.zeros((5, 2, 16, 128), dtype=torch.bfloat16)
+    bt, sl = torch.zeros((3, 8), dtype=torch.int32), torch.zeros(3, dtype=torch.int32)
+    for fn in (h, h.run_noalloc):
+        with pytest.raises(RldaError) as e:
+            fn(q, kv, kv, bt, sl)
+        assert e.value.status == -1 and "GPU" in str(e.value)
+    with pytest.raises(RldaError):
+        h.multi(q, kv, kv, bt, sl, torch.zeros(4, dtype=torch.int32))
+    with pytest.raises(RldaError):
+        h.append(torch.zeros((3, 2, 128), dtype=torch.bfloat16), None, kv, kv, bt, sl)

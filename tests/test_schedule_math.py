@@ -176,3 +176,4 @@ def test_xcd_share_map_is_a_bijection_with_contiguous_runs(W):
     for x in range(8):
         mine = sorted(s for b, s in enumerate(share) if b % 8 == x)
         assert mine == list(range(mine[0], mine[0] + len(mine))) if mine else True
+
