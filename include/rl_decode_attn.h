@@ -148,11 +148,11 @@ rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t handle, int32_t batch, 
  * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
  * allocation).  Same operation, kernel and arguments as rl_decode_attn_run, except:
  *   - the flags, segment counters and partial results live in a static device
- *     array of the library (about 4.3 MiB; one copy on each GPU the library runs
+ *     array of the library (about 8.6 MiB; one copy on each GPU the library runs
  *     on, held until the process ends), found on the first call on each device;
  *   - limits of that array: batch * num_kv_heads <= 65536 and head_dim <= 128
  *     (else RLDA_ERR_SCRATCH, nothing launched), and the work is cut into at most
- *     256 shares (one per CU on MI355X, the default);
+ *     512 shares (the default: one per CU on MI355X, two for fp8 caches);
  *   - flags: NULL, or a caller-owned device uint32_t (4-byte aligned) that receives
  *     the contract bits of rl_decode_attn_read_flags (OR-ed in; the caller clears
  *     it).  With NULL they go to a word of the static array that nothing reads.

@@ -225,10 +225,15 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32
   if (hipGetDevice(&dev) != hipSuccess) return RLDA_ERR_HIP;
   // One workgroup (one wave per SIMD) per CU by default: a second workgroup on a
   // CU would lose instruction arbitration to the first and finish its share later.
+  // fp8 pages are half the bytes of bf16 ones, and four waves per CU cannot keep
+  // enough of them in flight: plain fp8 runs of up to kTwoWgMaxBatch sequences take
+  // two workgroups per CU (two waves per SIMD, within 256 registers each).
+  const bool two = !grouped && h->kind == rlda::KvKind::FP8 && batch <= rlda::kTwoWgMaxBatch;
   int ranges = c.num_work_ranges;
   if (ranges == 0) {
     ranges = cu_count(dev);
     if (ranges <= 0) return RLDA_ERR_HIP;
+    if (two) ranges *= 2;
   }
   const int ranges_cap = mem ? mem->ranges_cap : h->ws_ranges;
   if (ranges > ranges_cap) ranges = ranges_cap;
@@ -269,8 +274,9 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32
   p.out_bf16 = c.out_dtype == RLDA_BF16;
   memcpy(p.q_head, h->q_head, sizeof p.q_head);
   if (!grouped) {
-    if (rlda::launch_decode(h->kind, c.head_dim, h->group, p, stream, ev_begin, ev_end) != hipSuccess)
-      return RLDA_ERR_HIP;
+    const int e = two ? rlda::launch_decode_two(h->kind, c.head_dim, p, stream, ev_begin, ev_end)
+                      : rlda::launch_decode(h->kind, c.head_dim, h->group, p, stream, ev_begin, ev_end);
+    if (e != hipSuccess) return RLDA_ERR_HIP;
     return RLDA_OK;
   }
   p.prefix_pages = prefix_pages;

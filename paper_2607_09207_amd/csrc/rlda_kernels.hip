@@ -771,6 +771,18 @@ __device__ __forceinline__ StreamChunk fetch_chunk(const Params& p, const int32_
 #endif
 constexpr bool kPromptTemporal = RLDA_PROMPT_TEMPORAL;
 
+// The prompt-pass state a grouped run's segment may start from (section 7b of the
+// attention kernel's users): only the launch that follows a prompt pass carries it.
+struct NoPromptState {};
+template <class Pol, bool PROMPT>
+struct PromptState {
+  typedef typename Pol::PInit type;
+};
+template <class Pol>
+struct PromptState<Pol, false> {
+  typedef NoPromptState type;
+};
+
 // MULTI: multi-token rows (rl_decode_attn_run_multi with at most 16 NT row_chunks
 // rows per (sequence, KV head)): (b, g) has n_b * G rows, row r is query head
 // (r % G) of query row q_start[b] + r / G and sees keys below L - n_b + r / G + 1;
@@ -780,8 +792,13 @@ constexpr bool kPromptTemporal = RLDA_PROMPT_TEMPORAL;
 // the rows of the tiles.  The units are packs instead of sequences; row r of a
 // pack is query head (r % G) of member r / G, and a page counts for every row (a
 // prompt page) or for one member's rows (its own pages).
-template <class Pol, bool MULTI = false, int NT = 1, bool PACK = false>
-__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(1, 1)))
+// PROMPT: the attention launch of a grouped run's prompt-pass form; a sequence's
+// first page then starts from the prompt pass's state.  Other launches carry no
+// prompt state (about 100 registers fewer).
+// WPE: waves per SIMD.  2: two workgroups per CU (batch <= kTwoWgMaxBatch, whose
+// per-sequence LDS tables leave room for two), each wave within 256 registers.
+template <class Pol, bool MULTI = false, int NT = 1, bool PACK = false, bool PROMPT = false, int WPE = 1>
+__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(WPE, WPE)))
 void decode_attention_kernel(const Params p) {
   static_assert(NT == 1 || (MULTI && NT == 2), "two row tiles only for multi-token rows");
   static_assert(!PACK || MULTI, "packed grouped runs use the multi-token row machinery");
@@ -791,7 +808,9 @@ void decode_attention_kernel(const Params p) {
   // threads per row, DPT output elements per thread.
   constexpr int kMR = 16 * NT, kTPR = kThreads / kMR;
   constexpr int DPT = D / kTPR;
-  constexpr int kB = PACK ? kPackMaxBatch : (NT == 2 ? kTwoTileMaxBatch : kMaxBatch);
+  static_assert(!(PROMPT && (MULTI || PACK)), "the prompt-pass state belongs to plain grouped launches");
+  static_assert(WPE == 1 || (WPE == 2 && !MULTI && !PACK && !PROMPT), "two waves per SIMD: plain runs only");
+  constexpr int kB = WPE == 2 ? kTwoWgMaxBatch : PACK ? kPackMaxBatch : (NT == 2 ? kTwoTileMaxBatch : kMaxBatch);
   // Units: sequences, or packs of group members (packed grouped runs).
   __shared__ int32_t s_pre[kB + 1];
   __shared__ uint8_t s_tail[kB];   // valid tokens of each sequence's last page
@@ -1037,7 +1056,8 @@ void decode_attention_kernel(const Params p) {
     Pol st, st2;   // st2: the second tile of a two-tile segment
     st.setup(p, lane, p.stride_slot);
     QN qring[kDepth];
-    typename Pol::PInit pring[kDepth];
+    typedef typename PromptState<Pol, PROMPT>::type PInit;
+    PInit pring[kDepth];
     bool began = false;   // the segment being accumulated began inside this quarter
     StreamChunk nxt = fetch_chunk<MULTI, PACK>(p, s_pre, s_tail, s_ppre, s_nfull, s_gpp, nunits, w0, w0, w1, lane, Hs, nrc);
     for (int base = w0; base < w1; base += kChunk) {
@@ -1051,7 +1071,7 @@ void decode_attention_kernel(const Params p) {
       float skm[kDepth], svm[kDepth];
       // Issue the loads of position base + k into pipeline slot `sl`.
       auto issue = [&](typename Pol::Frag& f, int& info_out, float& km_out, float& vm_out, QN& q_out,
-                       typename Pol::PInit& pi_out, int k) {
+                       PInit& pi_out, int k) {
         int pk = -1, info = 0;
         float ks = 1.f, vs = 1.f;
         if (k < cn) {
@@ -1094,7 +1114,7 @@ void decode_attention_kernel(const Params p) {
           if constexpr (NT == 2) Pol::load_q_multi(q_out.t[NT - 1], p, qs >> 5, qs & 31, g, rb + 16, lane, ld);
         } else if constexpr (Pol::kQRing) {
           Pol::load_q(q_out.t[0], p, b, g, lane, (info & (kInfoFirst | kInfoStart)) != 0);
-          Pol::load_prompt(pi_out, p, b, g, lane, (info & kInfoFirst) && (info & kInfoPrompt));
+          if constexpr (PROMPT) Pol::load_prompt(pi_out, p, b, g, lane, (info & kInfoFirst) && (info & kInfoPrompt));
         }
         info_out = info;   // the scales are used as loaded, in compute
         km_out = ks;
@@ -1102,12 +1122,12 @@ void decode_attention_kernel(const Params p) {
       };
       // Consume pipeline slot `sl` (position base + k).
       auto compute = [&](const typename Pol::Frag& f, int info, float km, float vm, const QN& q,
-                         const typename Pol::PInit& pi, int k) {
+                         const PInit& pi, int k) {
         if (k >= cn) return;
         const int g = (info >> kInfoHeadShift) & 255, b = (info >> kInfoSeqShift) & (PACK ? 4095 : 8191);
         if (info & (kInfoFirst | kInfoStart)) {
           bool seeded = false;
-          if constexpr (Pol::kQRing && !MULTI) {
+          if constexpr (Pol::kQRing && PROMPT) {
             if ((info & kInfoFirst) && (info & kInfoPrompt)) {
               st.begin_prompt(q.t[0], pi, G, lane);
               seeded = true;
@@ -1589,11 +1609,12 @@ int launch_append_t(const Params& p, void* stream) {
   return (int)hipGetLastError();
 }
 
-template <class Pol, bool MULTI = false, int NT = 1, bool PACK = false>
+template <class Pol, bool MULTI = false, int NT = 1, bool PACK = false, bool PROMPT = false, int WPE = 1>
 int launch(const Params& p, void* stream, void* ev_begin, void* ev_end) {
   hipStream_t st = (hipStream_t)stream;
   if (ev_begin && hipEventRecord((hipEvent_t)ev_begin, st) != hipSuccess) return -1;
-  hipLaunchKernelGGL((decode_attention_kernel<Pol, MULTI, NT, PACK>), dim3(p.nranges), dim3(kThreads), 0, st, p);
+  hipLaunchKernelGGL((decode_attention_kernel<Pol, MULTI, NT, PACK, PROMPT, WPE>), dim3(p.nranges), dim3(kThreads), 0, st,
+                     p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
   if (ev_end && hipEventRecord((hipEvent_t)ev_end, st) != hipSuccess) return -1;
@@ -1608,7 +1629,7 @@ int launch_prompt_then_decode(const Params& p, int ngroups, void* stream, void* 
   hipLaunchKernelGGL((prompt_kernel<D, FP8>), dim3(jobs * p.pfx_splits), dim3(kThreads), 0, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
-  return launch<Mfma<D, FP8>>(p, stream, nullptr, ev_end);
+  return launch<Mfma<D, FP8>, false, 1, false, true>(p, stream, nullptr, ev_end);
 }
 
 std::mutex g_scratch_mu;
@@ -1687,6 +1708,12 @@ int launch_decode_packed(KvKind kind, int head_dim, int tiles, const Params& p, 
       break;
   }
   return -1;
+}
+
+int launch_decode_two(KvKind kind, int head_dim, const Params& p, void* stream, void* ev_begin, void* ev_end) {
+  if (kind != KvKind::FP8) return -1;
+  return head_dim == 128 ? launch<Mfma<128, true>, false, 1, false, false, 2>(p, stream, ev_begin, ev_end)
+                         : launch<Mfma<64, true>, false, 1, false, false, 2>(p, stream, ev_begin, ev_end);
 }
 
 int launch_append(KvKind kind, int head_dim, const Params& p, void* stream) {
