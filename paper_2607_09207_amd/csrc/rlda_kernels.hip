@@ -680,7 +680,8 @@ struct Valu {
 // ---------------------------------------------------------------- stream metadata
 // A wave walks its quarter [w0, w1) of the flattened (sequence, KV head, page) list
 // as one continuous page stream.  Its lanes describe 64 consecutive positions at a
-// time (lane k: position base + k), fetched one chunk ahead of use.
+// time (lane k: position base + k), fetched one chunk ahead of use; the page ring
+// runs on across chunks.
 constexpr int kInfoTok = 31;            // valid tokens of the page (0: nothing to read)
 constexpr int kInfoFirst = 1 << 5;      // first page of its (sequence, KV head)
 constexpr int kInfoLast = 1 << 6;       // last page of its (sequence, KV head)
@@ -1059,24 +1060,33 @@ void decode_attention_kernel(const Params p) {
     typedef typename PromptState<Pol, PROMPT>::type PInit;
     PInit pring[kDepth];
     bool began = false;   // the segment being accumulated began inside this quarter
-    StreamChunk nxt = fetch_chunk<MULTI, PACK>(p, s_pre, s_tail, s_ppre, s_nfull, s_gpp, nunits, w0, w0, w1, lane, Hs, nrc);
-    for (int base = w0; base < w1; base += kChunk) {
-      const StreamChunk cur = nxt;
-      const int cn = min(kChunk, w1 - base);
-      if (base + kChunk < w1)
-        nxt = fetch_chunk<MULTI, PACK>(p, s_pre, s_tail, s_ppre, s_nfull, s_gpp, nunits, base + kChunk, w0, w1, lane,
-                                       Hs, nrc);
+    // Page ids and position info come kChunk positions per vector load: `cur` holds
+    // the chunk starting at position cbase, `nxt` the one after it (fetched a whole
+    // chunk ahead).  The ring runs across chunk boundaries, so it drains only at
+    // the end of the quarter.
+    const int cn = w1 - w0;   // positions of this quarter (relative index k)
+    auto fetch = [&](int base) {
+      return base < w1 ? fetch_chunk<MULTI, PACK>(p, s_pre, s_tail, s_ppre, s_nfull, s_gpp, nunits, base, w0, w1, lane,
+                                                  Hs, nrc)
+                       : StreamChunk{-1, 0};
+    };
+    StreamChunk cur = fetch(w0), nxt = fetch(w0 + kChunk);
+    int cbase = 0;   // relative position of cur's first entry
+    {
       typename Pol::Frag fr[kDepth];
       int sinfo[kDepth];
       float skm[kDepth], svm[kDepth];
-      // Issue the loads of position base + k into pipeline slot `sl`.
+      // Issue the loads of position w0 + k into pipeline slot `sl`.
       auto issue = [&](typename Pol::Frag& f, int& info_out, float& km_out, float& vm_out, QN& q_out,
                        PInit& pi_out, int k) {
         int pk = -1, info = 0;
         float ks = 1.f, vs = 1.f;
         if (k < cn) {
-          pk = __builtin_amdgcn_readlane(cur.pid, k);
-          info = __builtin_amdgcn_readlane(cur.info, k);
+          // Within two positions of the consumer, so at most one chunk ahead of it.
+          const bool in_cur = k < cbase + kChunk;
+          const int l = in_cur ? k - cbase : k - cbase - kChunk;
+          pk = __builtin_amdgcn_readlane(in_cur ? cur.pid : nxt.pid, l);
+          info = __builtin_amdgcn_readlane(in_cur ? cur.info : nxt.info, l);
           if ((unsigned)pk >= (unsigned)p.num_pages) {   // not a page of the pool: contributes nothing
             if (lane == 0) atomicOr(p.flags, kFlagBadPage);
             pk = -1;
@@ -1120,7 +1130,7 @@ void decode_attention_kernel(const Params p) {
         km_out = ks;
         vm_out = vs;
       };
-      // Consume pipeline slot `sl` (position base + k).
+      // Consume pipeline slot `sl` (position w0 + k).
       auto compute = [&](const typename Pol::Frag& f, int info, float km, float vm, const QN& q,
                          const PInit& pi, int k) {
         if (k >= cn) return;
@@ -1190,20 +1200,30 @@ void decode_attention_kernel(const Params p) {
           }
         }
       };
+      // Once position k (relative) is consumed: the last one of cur moves the ids on
+      // by a chunk (its successor has been read from nxt already).
+      auto advance = [&](int k) {
+        if (k + 1 == cbase + kChunk && k + 1 < cn) {
+          cur = nxt;
+          cbase += kChunk;
+          nxt = fetch(w0 + cbase + kChunk);
+        }
+      };
 #pragma unroll
       for (int k = 0; k < kDepth - 1; ++k)
         if (k < cn) issue(fr[k], sinfo[k], skm[k], svm[k], qring[k], pring[k], k);
       int i = 0;
-      // Steady state: every position issued lies inside the chunk.
+      // Steady state: every position issued lies inside the quarter.
       for (; i + 2 * kDepth - 2 < cn; i += kDepth) {
 #pragma unroll
         for (int k = 0; k < kDepth; ++k) {
           const int si = (k + kDepth - 1) % kDepth;
           issue(fr[si], sinfo[si], skm[si], svm[si], qring[si], pring[si], i + k + kDepth - 1);
           compute(fr[k], sinfo[k], skm[k], svm[k], qring[k], pring[k], i + k);
+          advance(i + k);
         }
       }
-      // Drain: no loads are issued past the chunk, so none is left in flight.
+      // Drain: no loads are issued past the quarter, so none is left in flight.
       for (; i < cn; i += kDepth) {
 #pragma unroll
         for (int k = 0; k < kDepth; ++k) {
@@ -1211,6 +1231,7 @@ void decode_attention_kernel(const Params p) {
           if (i + k + kDepth - 1 < cn)
             issue(fr[si], sinfo[si], skm[si], svm[si], qring[si], pring[si], i + k + kDepth - 1);
           compute(fr[k], sinfo[k], skm[k], svm[k], qring[k], pring[k], i + k);
+          advance(i + k);
         }
       }
     }
