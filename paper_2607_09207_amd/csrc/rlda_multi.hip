@@ -10,8 +10,9 @@
 // Work.  The query rows of one (sequence, KV head) are its n_b * G (token, query
 // head) pairs, token-major, so every K/V row read serves all G heads sharing that
 // KV head.  A workgroup takes 128 of them: each of its 4 waves owns one 32-row
-// MFMA tile.  Workgroups are numbered so that each sequence's last row blocks,
-// which attend to the most keys, are dispatched first.
+// MFMA tile.  Workgroups are numbered heaviest first over the whole call (the row
+// blocks that attend to the most keys are dispatched first), so the slots of the
+// GPU fill longest-job-first.
 //
 // Keys.  The workgroup walks its causal key range in blocks of 32 keys (two
 // pages).  Each wave brings one page of K or V of every block, two blocks ahead
@@ -128,68 +129,121 @@ void multi_query_kernel(const Params p) {
   __shared__ int32_t s_bad[S::NBUF][2 * kKH];   // page of the block not in the pool (contributes nothing)
   __shared__ int32_t s_scan[kWaves];
   __shared__ int16_t s_qh[kMaxQHeads];
-  extern __shared__ int32_t s_rb[];     // [batch + 1]: row blocks of the sequences before b
+  // Per sequence: {L - n_b (position of query token 0), n_b G rows} (rows 0 when
+  // its offsets are inconsistent).
+  extern __shared__ int2 s_sq[];   // [batch]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
   const int batch = p.batch, Hkv = p.num_kv_heads, G = p.group, Hq = p.num_q_heads;
   const int cap = p.max_pages * kPage;
 
-  // 1. Row blocks per sequence and their prefix sums (identical in every workgroup).
-  //    A sequence whose offsets are inconsistent gets none and raises the flag.
+  // 1. Rows of every sequence and the number of row blocks (identical in every
+  //    workgroup).  Inconsistent offsets give a sequence no rows; they, and lengths
+  //    out of range or shorter than the rows, raise the flag.
+  int nitems = 0;
   {
-    const int per = (batch + kThreads - 1) / kThreads;
-    const int lo = min(tid * per, batch), hi = min(lo + per, batch);
     int sum = 0, bad = 0;
-    for (int b = lo; b < hi; ++b) {
+    for (int b = tid; b < batch; b += kThreads) {
       const int q0 = p.q_start[b], q1 = p.q_start[b + 1];
       const bool ok = q0 >= 0 && q1 >= q0 && q1 <= p.total_q;
-      bad |= !ok;
-      const int nrb = ok ? (int)(((int64_t)(q1 - q0) * G + kMultiRows - 1) / kMultiRows) : 0;
-      s_rb[b + 1] = nrb;
-      sum += nrb;
+      const int n = ok ? q1 - q0 : 0;
+      int L = p.seq_lens[b];
+      if (!ok || L < 0 || L > cap || n > L) bad = 1;
+      L = min(max(L, 0), cap);
+      const int rows = (int)min((int64_t)n * G, (int64_t)INT32_MAX - kMultiRows);
+      s_sq[b] = make_int2(L - n, rows);
+      sum += (rows + kMultiRows - 1) / kMultiRows;
     }
-    if (bad && blockIdx.x == 0) atomicOr(p.flags, kFlagBadLen);
-    int x = sum;
+    if (__builtin_amdgcn_ballot_w64(bad) != 0 && blockIdx.x == 0 && lane == 0) atomicOr(p.flags, kFlagBadLen);
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(x, o);
-      if (lane >= o) x += y;
-    }
-    if (lane == 63) s_scan[wave] = x;
+    for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+    if (lane == 0) s_scan[wave] = sum;
     for (int e = tid; e < Hq; e += kThreads) s_qh[e] = p.q_head[e];
     __syncthreads();
-    int run = x - sum;
-    for (int w = 0; w < wave; ++w) run += s_scan[w];
-    for (int b = lo; b < hi; ++b) {
-      run += s_rb[b + 1];
-      s_rb[b + 1] = run;
-    }
-    if (tid == 0) s_rb[0] = 0;
-    __syncthreads();
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) nitems += s_scan[w];
   }
-  const int64_t items = (int64_t)s_rb[batch] * Hkv;
+  const int64_t items = (int64_t)nitems * Hkv;
   if (blockIdx.x == 0 && tid == 0 && items > (int64_t)gridDim.x) atomicOr(p.flags, kFlagBadLen);
   const int u = blockIdx.x;
   if (u >= items) return;
 
-  // 2. This workgroup's (sequence b, row block rb, KV head g).
-  const int g = u % Hkv, rbg = u / Hkv;
-  int b = 0;
+  // 2. This workgroup's (sequence b, row block rb, KV head g).  Row block rb of
+  //    sequence b covers rows [128 rb, r1), r1 = min(128 (rb + 1), n_b G), and reads
+  //    the keys below E = max(0, L - n_b + (r1 - 1) / G + 1), its cost.  The (row
+  //    block, KV head) items are dispatched heaviest first (keys descending; ties by
+  //    sequence, then last row block first), so the hardware's in-order dispatch
+  //    onto free slots packs them longest-job-first and the call does not end on a
+  //    long workgroup started late.  Item v = u / Hkv of that order is found by a
+  //    binary search on the key count: with C(x) the items having at least x keys
+  //    (a closed form per sequence, summed across the wave), its key count x* is the
+  //    largest x with C(x) > v.  Every wave finds it (no barrier).
+  const int g = u % Hkv, v = u / Hkv;
+  // Row blocks of sequence `sq` with at least x keys (E is non-decreasing in rb).
+  auto at_least = [&](int2 sq, int x) -> int {
+    const int rows = sq.y;
+    const int nrb = (rows + kMultiRows - 1) / kMultiRows;
+    const int64_t k = (int64_t)x - sq.x - 1;   // x >= 1: E >= x iff (r1 - 1) / G >= k
+    if (x <= 0 || k <= 0) return nrb;
+    const int64_t thr = (int64_t)G * k + 1;   // ... iff r1 >= thr
+    if (rows < thr) return 0;
+    return nrb - (int)((thr + kMultiRows - 1) / kMultiRows - 1);
+  };
+  auto count = [&](int x) {
+    int c = 0;
+    for (int b = lane; b < batch; b += 64) c += at_least(s_sq[b], x);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o);
+    return c;   // the same in every lane
+  };
+  int b = 0, rb = 0;
   {
-    int lo = 0, hi = batch;   // s_rb[lo] <= rbg < s_rb[hi]
+    int lo = 0, hi = cap + 1, chi = 0;   // C(lo) > v >= C(hi) = chi
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
-      if (s_rb[mid] <= rbg) lo = mid; else hi = mid;
+      const int c = count(mid);
+      if (c > v) {
+        lo = mid;
+      } else {
+        hi = mid;
+        chi = c;
+      }
     }
-    b = uni(lo);
+    // Among the items with exactly lo keys, the (v - chi)-th in sequence order.
+    int j = v - chi, found = 0;
+    for (int b0 = 0; b0 < batch && !found; b0 += 64) {
+      const int bb = b0 + lane;
+      int c1 = 0, c2 = 0, nrb = 0;
+      if (bb < batch) {
+        const int2 sq = s_sq[bb];
+        c1 = at_least(sq, lo);
+        c2 = at_least(sq, lo + 1);
+        nrb = (sq.y + kMultiRows - 1) / kMultiRows;
+      }
+      const int eq = c1 - c2;
+      int incl = eq;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (lane >= o) incl += y;
+      }
+      const uint64_t hit = __builtin_amdgcn_ballot_w64(j >= incl - eq && j < incl);
+      if (hit) {
+        const int src = __builtin_ctzll(hit);
+        b = __builtin_amdgcn_readlane(bb, src);
+        rb = __builtin_amdgcn_readlane(nrb - c2 - 1, src) - (j - __builtin_amdgcn_readlane(incl - eq, src));
+        found = 1;
+      } else {
+        j -= __builtin_amdgcn_readlane(incl, 63);
+      }
+    }
+    b = uni(b);
+    rb = uni(rb);
   }
-  const int rb = s_rb[b + 1] - 1 - rbg;               // the sequence's last row block first
-  const int q0 = p.q_start[b], n = p.q_start[b + 1] - q0;
-  int L = p.seq_lens[b];
-  if (L < 0 || L > cap || n > L) {
-    if (tid == 0) atomicOr(p.flags, kFlagBadLen);
-    L = min(max(L, 0), cap);
-  }
+  const int q0 = p.q_start[b];
+  const int2 sqb = s_sq[b];
+  const int n = sqb.y / G;
+  const int L = sqb.x + n;
   const int rows = n * G;
   const int r0 = rb * kMultiRows, r1 = min(r0 + kMultiRows, rows);
   const int base_pos = L - n;                                   // position of query token 0
@@ -580,7 +634,7 @@ template <int D, bool FP8>
 int launch_multi_t(const Params& p, int grid, void* stream, void* ev_begin, void* ev_end) {
   hipStream_t st = (hipStream_t)stream;
   if (ev_begin && hipEventRecord((hipEvent_t)ev_begin, st) != hipSuccess) return -1;
-  const size_t lds = sizeof(int32_t) * ((size_t)p.batch + 1);
+  const size_t lds = sizeof(int2) * (size_t)p.batch;
   hipLaunchKernelGGL((multi_query_kernel<D, FP8>), dim3(grid), dim3(kThreads), lds, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;
