@@ -22,6 +22,12 @@ constexpr int kPastRange = 0x40000000;       // buffer offset beyond any descrip
 
 __device__ __forceinline__ float neg_inf() { return -__builtin_huge_valf(); }
 
+// Workgroup barrier for data exchanged through LDS only: this wave's LDS operations
+// are complete, then s_barrier.  Unlike __syncthreads it does not wait for this
+// wave's global stores to complete.  The memory clobber keeps the compiler from
+// moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // Values equal in every lane, moved to scalar registers so that buffer
 // descriptors and loop bounds built from them stay scalar.
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }

@@ -832,6 +832,9 @@ void decode_attention_kernel(const Params p) {
   __shared__ int32_t s_last[2];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
+  // The query-head map (kernel argument memory), loaded alongside the lengths.
+  static_assert(kMaxQHeads <= kThreads, "one query head per thread");
+  const int16_t qh0 = tid < p.num_q_heads ? p.q_head[tid] : (int16_t)0;
   const int W = p.nranges;
   // Share index.  Workgroups are dispatched round-robin over the 8 XCDs (block b
   // runs on XCD b % 8); each XCD gets a contiguous run of shares, so neighbouring
@@ -945,7 +948,7 @@ void decode_attention_kernel(const Params p) {
       s_scan[wave] = x;
       s_scan_ne[wave] = xn;
     }
-    for (int e = tid; e < p.num_q_heads; e += kThreads) s_qhead[e] = p.q_head[e];
+    if (tid < p.num_q_heads) s_qhead[tid] = qh0;
     if (tid < 2 * kWaves) s_seg[tid] = -1;
     __syncthreads();
     int run = x - sum, rne = xn - cnt;
@@ -1070,7 +1073,7 @@ void decode_attention_kernel(const Params p) {
                                                   Hs, nrc)
                        : StreamChunk{-1, 0};
     };
-    StreamChunk cur = fetch(w0), nxt = fetch(w0 + kChunk);
+    StreamChunk cur = fetch(w0), nxt = {-1, 0};   // nxt: fetched once the first loads are out
     int cbase = 0;   // relative position of cur's first entry
     {
       typename Pol::Frag fr[kDepth];
@@ -1212,6 +1215,7 @@ void decode_attention_kernel(const Params p) {
 #pragma unroll
       for (int k = 0; k < kDepth - 1; ++k)
         if (k < cn) issue(fr[k], sinfo[k], skm[k], svm[k], qring[k], pring[k], k);
+      nxt = fetch(w0 + kChunk);   // first read kChunk - kDepth + 1 positions from now
       int i = 0;
       // Steady state: every position issued lies inside the quarter.
       for (; i + 2 * kDepth - 2 < cn; i += kDepth) {
@@ -1236,7 +1240,8 @@ void decode_attention_kernel(const Params p) {
       }
     }
   }
-  __syncthreads();
+  // The waves' pieces are in LDS; their global stores need not have completed.
+  lds_barrier();
 
   // 4. Merge the cut pieces in position order.  The used slots holding one segment
   //    are consecutive; together they are either the whole segment (normalise and
@@ -1261,14 +1266,31 @@ void decode_attention_kernel(const Params p) {
 #pragma unroll
     for (int e = 0; e < DPT; ++e) o[e] = 0.f;
     // Close the group of segment `cur`: write it, or publish this workgroup's piece.
+    // Lane j < 2 kWaves: slot j's segment and its first and last positions, read
+    // for every slot at once (the merge below takes them with readlane).
+    // Lane j < 2 kWaves: slot j's segment, its sequence and segment within the
+    // sequence, and its first and last positions, read for every slot at once (the
+    // merge below takes them with readlane).
+    int lseg = -2, lb = 0, lg = 0, lstart = 0, lend = 0;
+    if (lane < 2 * kWaves) {
+      lseg = s_seg[lane];
+      if (lseg >= 0) {
+        lb = lseg / Hs;
+        lg = lseg - lb * Hs;
+        const int pre_b = s_pre[lb], nb = s_pre[lb + 1] - pre_b;
+        lstart = Hs * pre_b + lg * nb;
+        lend = lstart + nb;
+      }
+    }
+    int jcur = 0;   // a slot of segment `cur`
+    int qh_cur = 0;   // this thread's output query head in segment `cur` (read when the group opens)
     auto flush = [&]() {
-      const int b = cur / Hs, g = cur - b * Hs;   // g: the segment within the sequence
-      const int pre_b = s_pre[b], nb = s_pre[b + 1] - pre_b;
-      const int64_t seg_start = (int64_t)Hs * pre_b + (int64_t)g * nb, seg_end = seg_start + nb;
+      const int b = __builtin_amdgcn_readlane(lb, jcur), g = __builtin_amdgcn_readlane(lg, jcur);
+      const int64_t seg_start = __builtin_amdgcn_readlane(lstart, jcur), seg_end = __builtin_amdgcn_readlane(lend, jcur);
       const bool whole = seg_start >= r0 && seg_end <= r1;
       if (h < seg_rows(b, g)) {
         if (whole) {
-          store_out<D, DPT>(p, out_row(b, g), out_head(g), d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
+          store_out<D, DPT>(p, out_row(b, g), qh_cur, d0, o, Ls > 0.f ? 1.f / Ls : 0.f);
         } else {
           const PartialRsrc rs = PartialRsrc::of<D>(p);
           const int gs = (seg_end > r1) ? 2 * u + 1 : 2 * u;
@@ -1284,30 +1306,40 @@ void decode_attention_kernel(const Params p) {
       }
       if (!whole && nhand < 2) hand_seg[nhand++] = cur;   // only the first and last group can be cut
     };
-    // Slots in position order; the used slots of one segment are consecutive.  Each
-    // step issues its LDS reads (tag, max/sum, partial output) together.
+    // Slots in position order; the used slots of one segment are consecutive.  The
+    // LDS reads of slot j + 1 (max/sum, partial output) are issued before slot j is
+    // merged, so their latency overlaps the merge and the stores.
+    float mn, ln, vn[DPT];
+    auto load_slot = [&](int j) {
+      mn = s_ml[j][h][0];
+      ln = s_ml[j][h][1];
+#pragma unroll
+      for (int c = 0; c < DPT; c += 4) *(f32x4*)&vn[c] = *(const f32x4*)&s_acc[j][h][d0 + c];
+    };
+    load_slot(0);
 #pragma unroll 1
     for (int j = 0; j <= 2 * kWaves; ++j) {
       int sj = -2;   // -2: past the last slot
-      float mj = neg_inf(), lj = 0.f, v[DPT];
-      if (j < 2 * kWaves) {
-        sj = s_seg[j];
-        mj = s_ml[j][h][0];
-        lj = s_ml[j][h][1];
+      float mj = mn, lj = ln, v[DPT];
 #pragma unroll
-        for (int c = 0; c < DPT; c += 4) *(f32x4*)&v[c] = *(const f32x4*)&s_acc[j][h][d0 + c];
+      for (int e = 0; e < DPT; ++e) v[e] = vn[e];
+      if (j < 2 * kWaves) {
+        sj = __builtin_amdgcn_readlane(lseg, j);
+        if (j + 1 < 2 * kWaves) load_slot(j + 1);
       }
-      sj = uni(sj);
       if (sj == -1) continue;   // unused slot
       if (sj != cur) {
         if (cur >= 0) flush();
         cur = sj;
+        jcur = j;
+        if (sj >= 0) qh_cur = out_head(__builtin_amdgcn_readlane(lg, j));
         M = neg_inf();
         Ls = 0.f;
 #pragma unroll
         for (int e = 0; e < DPT; ++e) o[e] = 0.f;
       }
-      if (sj >= 0 && h < seg_rows(sj / Hs, sj - (sj / Hs) * Hs)) lse_merge<DPT>(M, Ls, o, mj, lj, v);
+      if (sj >= 0 && h < seg_rows(__builtin_amdgcn_readlane(lb, j), __builtin_amdgcn_readlane(lg, j)))
+        lse_merge<DPT>(M, Ls, o, mj, lj, v);
     }
   }
 
