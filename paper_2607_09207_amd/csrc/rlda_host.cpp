@@ -528,7 +528,9 @@ rlda_status rl_decode_attn_run_multi(rl_decode_attn_t h, int32_t batch, int32_t 
   // One workgroup per (row block, KV head): a sequence's n_b * G rows take at most
   // n_b * G / rows_per_block + 1 blocks, so this grid covers every consistent q_start.
   const int64_t blocks = ((int64_t)total_q * h->group + rlda::kMultiRows - 1) / rlda::kMultiRows + batch;
-  const int64_t grid = blocks * c.num_kv_heads;
+  // Four KV heads: each XCD takes one KV head of one of two sequence classes, and
+  // the grid holds 8 blocks per row block so that either class fits (see the kernel).
+  const int64_t grid = blocks * (c.num_kv_heads == 4 ? 8 : c.num_kv_heads);
   if (grid > INT32_MAX) return RLDA_ERR_UNSUPPORTED;
   if (rlda::launch_multi(h->kind, c.head_dim, p, (int)grid, stream, event_begin, event_end) != hipSuccess)
     return RLDA_ERR_HIP;

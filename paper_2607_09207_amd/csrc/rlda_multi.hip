@@ -129,6 +129,7 @@ void multi_query_kernel(const Params p) {
   __shared__ int32_t s_bad[S::NBUF][2 * kKH];   // page of the block not in the pool (contributes nothing)
   __shared__ int32_t s_scan[kWaves];
   __shared__ int16_t s_qh[kMaxQHeads];
+  __shared__ uint8_t s_cls[64];   // sequence classes (XCD placement, batches of at most 64)
   // Per sequence: {L - n_b (position of query token 0), n_b G rows} (rows 0 when
   // its offsets are inconsistent).
   extern __shared__ int2 s_sq[];   // [batch]
@@ -165,20 +166,65 @@ void multi_query_kernel(const Params p) {
   }
   const int64_t items = (int64_t)nitems * Hkv;
   if (blockIdx.x == 0 && tid == 0 && items > (int64_t)gridDim.x) atomicOr(p.flags, kFlagBadLen);
-  const int u = blockIdx.x;
-  if (u >= items) return;
 
-  // 2. This workgroup's (sequence b, row block rb, KV head g).  Row block rb of
-  //    sequence b covers rows [128 rb, r1), r1 = min(128 (rb + 1), n_b G), and reads
-  //    the keys below E = max(0, L - n_b + (r1 - 1) / G + 1), its cost.  The (row
-  //    block, KV head) items are dispatched heaviest first (keys descending; ties by
-  //    sequence, then last row block first), so the hardware's in-order dispatch
-  //    onto free slots packs them longest-job-first and the call does not end on a
-  //    long workgroup started late.  Item v = u / Hkv of that order is found by a
-  //    binary search on the key count: with C(x) the items having at least x keys
-  //    (a closed form per sequence, summed across the wave), its key count x* is the
-  //    largest x with C(x) > v.  Every wave finds it (no barrier).
-  const int g = u % Hkv, v = u / Hkv;
+  // 2. The (sequence b, row block rb, KV head g) items of this workgroup.  Row block
+  //    rb of sequence b covers rows [128 rb, r1), r1 = min(128 (rb + 1), n_b G), and
+  //    reads the keys below E = max(0, L - n_b + (r1 - 1) / G + 1), its cost.
+  //    Placement: workgroups are dispatched round-robin over the 8 XCDs (block u on
+  //    XCD u % 8), and the row blocks of one (sequence, KV head) read the same pages,
+  //    so they are kept on one XCD, whose L2 then serves the repeats:
+  //      Hkv a multiple of 8: XCD x takes KV heads x, x + 8, ... of every sequence;
+  //      Hkv = 4:             XCD x takes KV head x % 4 of the sequences of class
+  //                           x / 4, the two classes balanced by work (rank by
+  //                           estimated keys, snake order; batches above 64: b mod 2),
+  //                           the grid holding 8 blocks per (sequence, row block) so
+  //                           that either class fits;
+  //      otherwise:           one set over the whole grid, no placement.
+  //    Within its set each XCD dispatches heaviest first (keys descending; ties by
+  //    sequence, then last row block first, then KV head), so the slots of the XCD
+  //    fill longest-job-first; block t of the XCD takes item t of its set (blocks
+  //    past the set's end return).  Item t is found by a binary search on the key count: with
+  //    C(x) the items having at least x keys (a closed form per sequence, summed
+  //    across the wave), its key count x* is the largest x with C(x) > t.  Every wave
+  //    finds it (no barrier).
+  const int u = blockIdx.x, xcd = u & 7;
+  const bool by_head = Hkv % 8 == 0, by_class = Hkv == 4;
+  const int ncls = by_class ? 8 / Hkv : 1, my_cls = by_class ? xcd / Hkv : 0;
+  const int hx = by_head ? Hkv / 8 : (by_class ? 1 : Hkv);   // KV heads per (b, rb) in the set
+  const int g_base = by_head ? xcd : (by_class ? xcd % Hkv : 0), g_step = by_head ? 8 : 1;
+  const int t_first = (by_head || by_class) ? u >> 3 : u;
+  if (by_class && batch <= 64) {
+    // Class of each sequence: sort by estimated keys (descending; bitonic across the
+    // lanes of wave 0), then deal the ranks out in snake order 0, 1, .., K-1, K-1, .., 0.
+    if (wave == 0) {
+      float key = -1.f;
+      int id = lane;
+      if (lane < batch) {
+        const int2 sq = s_sq[lane];
+        const int nrb = (sq.y + kMultiRows - 1) / kMultiRows;
+        key = (float)nrb * ((float)max(sq.x, 0) + 0.5f * (float)(sq.y / G) + 1.f);
+      }
+#pragma unroll
+      for (int k = 2; k <= 64; k <<= 1)
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1) {
+          const float ok = __shfl_xor(key, j);
+          const int oid = __shfl_xor(id, j);
+          const bool mine_first = key > ok || (key == ok && id < oid);
+          const bool keep = (((lane & j) == 0) == ((lane & k) == 0)) ? mine_first : !mine_first;
+          if (!keep) {
+            key = ok;
+            id = oid;
+          }
+        }
+      const int rr = lane % (2 * ncls);
+      if (id < batch) s_cls[id] = (uint8_t)(rr < ncls ? rr : 2 * ncls - 1 - rr);
+    }
+    __syncthreads();
+  }
+  auto in_set = [&](int b) {
+    return !by_class || (batch <= 64 ? (int)s_cls[b] : b % ncls) == my_cls;
+  };
   // Row blocks of sequence `sq` with at least x keys (E is non-decreasing in rb).
   auto at_least = [&](int2 sq, int x) -> int {
     const int rows = sq.y;
@@ -191,11 +237,16 @@ void multi_query_kernel(const Params p) {
   };
   auto count = [&](int x) {
     int c = 0;
-    for (int b = lane; b < batch; b += 64) c += at_least(s_sq[b], x);
+    for (int b = lane; b < batch; b += 64)
+      if (in_set(b)) c += at_least(s_sq[b], x);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o);
     return c;   // the same in every lane
   };
+  const int set_items = count(0) * hx;
+
+  if (t_first >= set_items) return;
+  const int v = t_first / hx, g = g_base + g_step * (t_first - v * hx);
   int b = 0, rb = 0;
   {
     int lo = 0, hi = cap + 1, chi = 0;   // C(lo) > v >= C(hi) = chi
@@ -214,7 +265,7 @@ void multi_query_kernel(const Params p) {
     for (int b0 = 0; b0 < batch && !found; b0 += 64) {
       const int bb = b0 + lane;
       int c1 = 0, c2 = 0, nrb = 0;
-      if (bb < batch) {
+      if (bb < batch && in_set(bb)) {
         const int2 sq = s_sq[bb];
         c1 = at_least(sq, lo);
         c2 = at_least(sq, lo + 1);
