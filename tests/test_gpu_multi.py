@@ -149,6 +149,20 @@ def test_multi_is_bitwise_deterministic(torch_cuda):
     assert np.array_equal(a, b)
 
 
+@pytest.mark.parametrize("Hq,Hkv,B", [(28, 4, 80), (32, 16, 5), (8, 8, 70)], ids=["Hkv4-B80", "Hkv16-B5", "Hkv8-B70"])
+def test_multi_every_xcd_placement(torch_cuda, Hq, Hkv, B):
+    """The 128-row kernel's item placements: four KV heads with more than 64 sequences
+    (classes by sequence index), sixteen (two KV heads per XCD) and eight with many
+    sequences; every output against the oracle."""
+    rng = np.random.default_rng(81 + Hkv)
+    lens = rng.integers(1, 700, size=B)
+    ql = np.minimum(rng.integers(0, 160, size=B), lens)
+    w = I.make_multi(lens.tolist(), ql.tolist(), Hq, Hkv, 64, q_dtype="bf16", kv_dtype="bf16", seed=82)
+    got, flags = run_multi(torch_cuda, w, tag=f"placement Hkv={Hkv} B={B}")
+    assert flags == 0
+    assert_close(got, oracle.run_multi(w), "bf16", f"multi placement Hkv={Hkv} B={B}")
+
+
 def test_maximum_batch_multi(torch_cuda):
     """The multi-token entry point's largest batch (4096) with 0-3 rows per sequence."""
     rng = np.random.default_rng(79)
