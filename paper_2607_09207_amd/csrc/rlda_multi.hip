@@ -127,23 +127,26 @@ void multi_query_kernel(const Params p) {
   __shared__ __align__(16) char s_v[S::NBUF][kKeys * S::VRS];
   __shared__ float s_scale[S::NBUF][4 * kKH];   // fp8: K scales of the block's pages, then V's
   __shared__ int32_t s_bad[S::NBUF][2 * kKH];   // page of the block not in the pool (contributes nothing)
-  __shared__ int32_t s_scan[kWaves];
+  __shared__ int32_t s_scan[kWaves], s_emax[kWaves];
   __shared__ int16_t s_qh[kMaxQHeads];
   __shared__ uint8_t s_cls[64];   // sequence classes (XCD placement, batches of at most 64)
   // Per sequence: {L - n_b (position of query token 0), n_b G rows} (rows 0 when
   // its offsets are inconsistent).
-  extern __shared__ int2 s_sq[];   // [batch]
+  extern __shared__ int2 s_sq[];   // [batch], then s_key [batch]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
   const int batch = p.batch, Hkv = p.num_kv_heads, G = p.group, Hq = p.num_q_heads;
   const int cap = p.max_pages * kPage;
+  // Ordering key of each sequence's row blocks: its key count L when they are
+  // dispatched together, -1 when each row block is ordered by its own key count.
+  int32_t* s_key = (int32_t*)(s_sq + batch);
 
   // 1. Rows of every sequence and the number of row blocks (identical in every
   //    workgroup).  Inconsistent offsets give a sequence no rows; they, and lengths
   //    out of range or shorter than the rows, raise the flag.
-  int nitems = 0;
+  int nitems = 0, emax = 0;   // emax: the most keys any sequence's rows see
   {
-    int sum = 0, bad = 0;
+    int sum = 0, bad = 0, lmax = 0;
     for (int b = tid; b < batch; b += kThreads) {
       const int q0 = p.q_start[b], q1 = p.q_start[b + 1];
       const bool ok = q0 >= 0 && q1 >= q0 && q1 <= p.total_q;
@@ -154,15 +157,33 @@ void multi_query_kernel(const Params p) {
       const int rows = (int)min((int64_t)n * G, (int64_t)INT32_MAX - kMultiRows);
       s_sq[b] = make_int2(L - n, rows);
       sum += (rows + kMultiRows - 1) / kMultiRows;
+      if (rows > 0) lmax = max(lmax, L);
     }
     if (__builtin_amdgcn_ballot_w64(bad) != 0 && blockIdx.x == 0 && lane == 0) atomicOr(p.flags, kFlagBadLen);
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
-    if (lane == 0) s_scan[wave] = sum;
+    for (int o = 32; o >= 1; o >>= 1) {
+      sum += __shfl_xor(sum, o);
+      lmax = max(lmax, __shfl_xor(lmax, o));
+    }
+    if (lane == 0) {
+      s_scan[wave] = sum;
+      s_emax[wave] = lmax;
+    }
     for (int e = tid; e < Hq; e += kThreads) s_qh[e] = p.q_head[e];
     __syncthreads();
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) nitems += s_scan[w];
+    for (int w = 0; w < kWaves; ++w) {
+      nitems += s_scan[w];
+      emax = max(emax, s_emax[w]);
+    }
+    // A sequence whose rows see at most an eighth of the largest job's keys apart
+    // is dispatched as a group (its row blocks then read its pages together).
+    for (int b = tid; b < batch; b += kThreads) {
+      const int2 sq = s_sq[b];
+      const int n = sq.y / G;
+      s_key[b] = (sq.y > 0 && 8 * (int64_t)n <= emax) ? max(0, sq.x + n) : -1;
+    }
+    __syncthreads();
   }
   const int64_t items = (int64_t)nitems * Hkv;
   if (blockIdx.x == 0 && tid == 0 && items > (int64_t)gridDim.x) atomicOr(p.flags, kFlagBadLen);
@@ -182,7 +203,9 @@ void multi_query_kernel(const Params p) {
   //      otherwise:           one set over the whole grid, no placement.
   //    Within its set each XCD dispatches heaviest first (keys descending; ties by
   //    sequence, then last row block first, then KV head), so the slots of the XCD
-  //    fill longest-job-first; block t of the XCD takes item t of its set (blocks
+  //    fill longest-job-first.  The row blocks of a sequence whose rows span at most
+  //    an eighth of the largest job's keys all take the sequence's key count L: they
+  //    run together and read the sequence's pages side by side, once from HBM; block t of the XCD takes item t of its set (blocks
   //    past the set's end return).  Item t is found by a binary search on the key count: with
   //    C(x) the items having at least x keys (a closed form per sequence, summed
   //    across the wave), its key count x* is the largest x with C(x) > t.  Every wave
@@ -226,11 +249,13 @@ void multi_query_kernel(const Params p) {
     return !by_class || (batch <= 64 ? (int)s_cls[b] : b % ncls) == my_cls;
   };
   // Row blocks of sequence `sq` with at least x keys (E is non-decreasing in rb).
-  auto at_least = [&](int2 sq, int x) -> int {
+  auto at_least = [&](int2 sq, int key, int x) -> int {
     const int rows = sq.y;
     const int nrb = (rows + kMultiRows - 1) / kMultiRows;
+    if (x <= 0) return nrb;
+    if (key >= 0) return key >= x ? nrb : 0;   // dispatched as a group
     const int64_t k = (int64_t)x - sq.x - 1;   // x >= 1: E >= x iff (r1 - 1) / G >= k
-    if (x <= 0 || k <= 0) return nrb;
+    if (k <= 0) return nrb;
     const int64_t thr = (int64_t)G * k + 1;   // ... iff r1 >= thr
     if (rows < thr) return 0;
     return nrb - (int)((thr + kMultiRows - 1) / kMultiRows - 1);
@@ -238,7 +263,7 @@ void multi_query_kernel(const Params p) {
   auto count = [&](int x) {
     int c = 0;
     for (int b = lane; b < batch; b += 64)
-      if (in_set(b)) c += at_least(s_sq[b], x);
+      if (in_set(b)) c += at_least(s_sq[b], s_key[b], x);
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o);
     return c;   // the same in every lane
@@ -267,8 +292,9 @@ void multi_query_kernel(const Params p) {
       int c1 = 0, c2 = 0, nrb = 0;
       if (bb < batch && in_set(bb)) {
         const int2 sq = s_sq[bb];
-        c1 = at_least(sq, lo);
-        c2 = at_least(sq, lo + 1);
+        const int key = s_key[bb];
+        c1 = at_least(sq, key, lo);
+        c2 = at_least(sq, key, lo + 1);
         nrb = (sq.y + kMultiRows - 1) / kMultiRows;
       }
       const int eq = c1 - c2;
@@ -685,7 +711,7 @@ template <int D, bool FP8>
 int launch_multi_t(const Params& p, int grid, void* stream, void* ev_begin, void* ev_end) {
   hipStream_t st = (hipStream_t)stream;
   if (ev_begin && hipEventRecord((hipEvent_t)ev_begin, st) != hipSuccess) return -1;
-  const size_t lds = sizeof(int2) * (size_t)p.batch;
+  const size_t lds = (sizeof(int2) + sizeof(int32_t)) * (size_t)p.batch;
   hipLaunchKernelGGL((multi_query_kernel<D, FP8>), dim3(grid), dim3(kThreads), lds, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return (int)e;

@@ -126,7 +126,7 @@ int launch_decode_packed(KvKind kind, int head_dim, int tiles, const Params& p, 
 #endif
 constexpr int kMultiTiles = RLDA_MQ_TILES;
 constexpr int kMultiRows = 128 * kMultiTiles;   // query rows (token, head pairs) per workgroup of the multi-token kernel
-constexpr int kMultiMaxBatch = 4096;   // its per-sequence LDS table stays within 32 KiB of LDS per workgroup
+constexpr int kMultiMaxBatch = 4096;   // its per-sequence LDS tables stay within 48 KiB of LDS per workgroup
 constexpr int kPackMaxBatch = 4096;    // packed grouped runs: per-sequence and per-pack LDS tables of this size
 constexpr int kPackMaxMembers = 7;     // ... members per pack (3 bits of the page descriptor, 7 = every member)
 constexpr int kPackMaxPages = 32767;   // ... pages per sequence (16-bit LDS entries)
