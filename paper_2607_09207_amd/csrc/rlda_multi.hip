@@ -194,9 +194,10 @@ void multi_query_kernel(const Params p) {
   //    Placement: workgroups are dispatched round-robin over the 8 XCDs (block u on
   //    XCD u % 8), and the row blocks of one (sequence, KV head) read the same pages,
   //    so they are kept on one XCD, whose L2 then serves the repeats:
-  //      Hkv a multiple of 8: XCD x takes KV heads x, x + 8, ... of every sequence;
-  //      Hkv = 4:             XCD x takes KV head x % 4 of the sequences of class
-  //                           x / 4, the two classes balanced by work (rank by
+  //      Hkv a multiple of 8: XCD x takes KV heads (x + b) % 8, + 8, ... of every
+  //                           sequence b;
+  //      Hkv = 4:             XCD x takes KV head (x + b) % 4 of the sequences b of
+  //                           class x / 4, the two classes balanced by work (rank by
   //                           estimated keys, snake order; batches above 64: b mod 2),
   //                           the grid holding 8 blocks per (sequence, row block) so
   //                           that either class fits;
@@ -214,7 +215,6 @@ void multi_query_kernel(const Params p) {
   const bool by_head = Hkv % 8 == 0, by_class = Hkv == 4;
   const int ncls = by_class ? 8 / Hkv : 1, my_cls = by_class ? xcd / Hkv : 0;
   const int hx = by_head ? Hkv / 8 : (by_class ? 1 : Hkv);   // KV heads per (b, rb) in the set
-  const int g_base = by_head ? xcd : (by_class ? xcd % Hkv : 0), g_step = by_head ? 8 : 1;
   const int t_first = (by_head || by_class) ? u >> 3 : u;
   if (by_class && batch <= 64) {
     // Class of each sequence: sort by estimated keys (descending; bitonic across the
@@ -271,7 +271,7 @@ void multi_query_kernel(const Params p) {
   const int set_items = count(0) * hx;
 
   if (t_first >= set_items) return;
-  const int v = t_first / hx, g = g_base + g_step * (t_first - v * hx);
+  const int v = t_first / hx, hsub = t_first - v * hx;
   int b = 0, rb = 0;
   {
     int lo = 0, hi = cap + 1, chi = 0;   // C(lo) > v >= C(hi) = chi
@@ -317,6 +317,9 @@ void multi_query_kernel(const Params p) {
     b = uni(b);
     rb = uni(rb);
   }
+  // The KV head: rotated by the sequence, so that every XCD serves every head (the
+  // head fixes the page tiles' offset, and with it their HBM channels).
+  const int g = by_head ? ((xcd + b) & 7) + 8 * hsub : (by_class ? (xcd + b) % Hkv : hsub);
   const int q0 = p.q_start[b];
   const int2 sqb = s_sq[b];
   const int n = sqb.y / G;
