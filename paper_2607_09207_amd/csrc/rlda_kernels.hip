@@ -715,13 +715,19 @@ template <bool MULTI, bool PACK>
 __device__ __forceinline__ StreamChunk fetch_chunk(const Params& p, const int32_t* s_pre, const uint8_t* s_tail,
                                                    const int32_t* s_ppre, const uint16_t* s_nfull,
                                                    const int16_t* s_gpp, int nunits, int base, int w0, int w1,
-                                                   int lane, int Hs, int nrc) {
+                                                   int lane, int Hs, int nrc, int hint) {
   StreamChunk c = {-1, 0};
   const int pos = base + lane;
   if (pos < w1) {
     const int y = (int)((uint32_t)pos / (uint32_t)Hs);
-    int lo = 0, hi = nunits;   // s_pre[lo] <= y < s_pre[hi]
-    while (hi - lo > 1) {
+    // `hint` is the unit of a position at or before `base`, so s_pre[hint] <= y.  A
+    // chunk spans few units: gallop from it, then bisect.
+    int lo = hint, hi = min(nunits, hint + 1);
+    for (int step = 2; hi < nunits && s_pre[hi] <= y; step <<= 1) {
+      lo = hi;
+      hi = min(nunits, lo + step);
+    }
+    while (hi - lo > 1) {   // s_pre[lo] <= y < s_pre[hi]
       const int mid = (lo + hi) >> 1;
       if (s_pre[mid] <= y) lo = mid; else hi = mid;
     }
@@ -855,87 +861,46 @@ void decode_attention_kernel(const Params p) {
 
   // Units of the flattened list: sequences, or packs (packed grouped runs).
   const int nunits = PACK ? p.pack_units : batch;
+  // Packed grouped runs whose groups are aligned runs of the lanes (a power-of-two
+  // group size up to 64 dividing the batch, a power-of-two pack size dividing it,
+  // at most one sequence per thread): the group clamps and the pack sums are
+  // shuffles across the members' lanes, so the prologue needs one barrier before
+  // the scan instead of three.  Other shapes take the general prologue below.
+  bool pack_lanes = false;
   if constexpr (PACK) {
-    // Pages and last-page tokens of every sequence, then each group's prompt pages:
-    // the requested count clamped to the full pages of its shortest member.  The
-    // first requested counts are loaded together with the lengths.
-    const int gs = p.group_size, ngroups = (batch + gs - 1) / gs;
-    const int want0 = tid < ngroups ? p.prefix_pages[tid] : 0;
-    int bad = 0;
-    for (int b = tid; b < batch; b += kThreads) {
-      int L = p.seq_lens[b];
-      if (L < 0 || L > cap) bad = 1;
-      L = min(max(L, 0), cap);
-      const int nf = (L + kPage - 1) / kPage;
-      s_nfull[b] = (uint16_t)nf;
-      s_tail[b] = (uint8_t)(L - (nf - 1) * kPage);
-    }
-    if (bad && u == 0) atomicOr(p.flags, kFlagBadLen);
-    __syncthreads();
-    for (int i = tid; i < ngroups; i += kThreads) {
-      int mn = 0x7fffffff;
-      for (int b = i * gs; b < min(batch, (i + 1) * gs); ++b) {
-        const int nf = s_nfull[b];
-        mn = min(mn, (nf > 0 && s_tail[b] < kPage) ? nf - 1 : nf);   // full pages
-      }
-      const int want = i == tid ? want0 : p.prefix_pages[i], pp = max(0, min(want, mn));
-      if (want != pp && u == 0) atomicOr(p.flags, kFlagPrefixClamped);
-      s_gpp[i] = (int16_t)pp;
-    }
-    __syncthreads();
+    const int gs = p.group_size, P = p.pack;
+    pack_lanes = batch <= kThreads && gs <= 64 && (gs & (gs - 1)) == 0 && P >= 1 && (P & (P - 1)) == 0 && P <= gs &&
+                 batch % gs == 0 && nunits * P == batch;
   }
-
-  // 1. Page counts per unit and their prefix sums (identical in every workgroup).
-  {
-    const int per = (nunits + kThreads - 1) / kThreads;
-    const int lo = min(tid * per, nunits), hi = min(lo + per, nunits);
-    int sum = 0, cnt = 0, bad = 0;   // pages, non-empty units
-    for (int b = lo; b < hi; ++b) {
-      if constexpr (PACK) {
-        // Pack b: members b0 .. b0 + np - 1 of group i; the prompt once, then each member's own pages.
-        const int gs = p.group_size, P = p.pack, ppg = (gs + P - 1) / P;
-        const int i = b / ppg, r = b - i * ppg;
-        const int b0 = i * gs + r * P, np = min(P, min(batch, (i + 1) * gs) - b0);
-        const int pp = s_gpp[i];
-        int n = pp;
-        for (int m = 0; m < np; ++m) n += s_nfull[b0 + m] - pp;
-        s_ppre[b] = (b0 << 5) | np;
-        s_pre[b + 1] = n;
-        sum += n;
-        cnt += n > 0;
-        continue;
-      }
-      int L = p.seq_lens[b];
-      if (L < 0 || L > cap) bad = 1;
-      L = min(max(L, 0), cap);
-      int nfull = (L + kPage - 1) / kPage;
-      int pp = 0;
-      if constexpr (MULTI) {
-        // Inconsistent offsets, or more rows than the call allows: no rows.  More
-        // rows than tokens: flagged; rows before position 0 see no key (zeros).
-        const int q0 = p.q_start[b], q1 = p.q_start[b + 1];
-        int nq = q1 - q0;
-        if (q0 < 0 || q1 < q0 || q1 > p.total_q || nq > p.max_q_len) {
-          bad = 1;
-          nq = 0;
-        }
-        if (nq > L) bad = 1;
-        if (nq == 0) nfull = 0;
-        s_ppre[b] = nq > 0 ? (q0 << 5) | nq : 0;
-      } else {
-        // Grouped runs: the prompt pass covered the first pp pages (its clamp keeps
-        // pp <= floor(L / 16)); this kernel streams the rest.
-        pp = p.group_size > 0 ? min(max(p.gprefix[b / p.group_size], 0), L / kPage) : 0;
-        s_ppre[b] = pp;
-      }
-      const int n = nfull - pp;
-      s_pre[b + 1] = n;
-      s_tail[b] = (uint8_t)(L - (nfull - 1) * kPage);   // 1..16 when nfull > 0
-      sum += n;
-      cnt += n > 0;
+  if (PACK && pack_lanes) {
+    const int gs = p.group_size, P = p.pack, b = tid;
+    const bool live = b < batch;
+    int L = live ? p.seq_lens[b] : 0;
+    const int want = live ? p.prefix_pages[b / gs] : 0;
+    const bool badl = live && (L < 0 || L > cap);
+    L = min(max(L, 0), cap);
+    const int nf = (L + kPage - 1) / kPage, tail = L - (nf - 1) * kPage;
+    // The group's prompt: the requested pages clamped to its shortest member's full pages.
+    int mn = live ? ((nf > 0 && tail < kPage) ? nf - 1 : nf) : 0x7fffffff;
+    for (int o = 1; o < gs; o <<= 1) mn = min(mn, __shfl_xor(mn, o));
+    const int pp = max(0, min(want, mn));
+    // Pack b / P: the prompt once, then each member's own pages.
+    int own = live ? nf - pp : 0;
+    for (int o = 1; o < P; o <<= 1) own += __shfl_xor(own, o);
+    const bool head = live && (b & (P - 1)) == 0;   // the lane of the pack's first member
+    const int n = head ? pp + own : 0;
+    if (live) {
+      s_nfull[b] = (uint16_t)nf;
+      s_tail[b] = (uint8_t)tail;
+      if ((b & (gs - 1)) == 0) s_gpp[b / gs] = (int16_t)pp;
     }
-    if (bad && u == 0) atomicOr(p.flags, kFlagBadLen);
-    int x = sum, xn = cnt;
+    if (head) s_ppre[b / P] = (b << 5) | P;
+    if (__builtin_amdgcn_ballot_w64(badl) != 0 && lane == 0 && u == 0) atomicOr(p.flags, kFlagBadLen);
+    if (__builtin_amdgcn_ballot_w64(live && (b & (gs - 1)) == 0 && want != pp) != 0 && lane == 0 && u == 0)
+      atomicOr(p.flags, kFlagPrefixClamped);
+    // Prefix sums of the packs' pages and of the non-empty packs, in pack order
+    // (= lane order of the packs' first members).
+    int x = n, xn = n > 0;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
       const int y = __shfl_up(x, o), yn = __shfl_up(xn, o);
@@ -951,24 +916,137 @@ void decode_attention_kernel(const Params p) {
     if (tid < p.num_q_heads) s_qhead[tid] = qh0;
     if (tid < 2 * kWaves) s_seg[tid] = -1;
     __syncthreads();
-    int run = x - sum, rne = xn - cnt;
+    int run = x, rne = xn;   // inclusive
     for (int w = 0; w < wave; ++w) {
       run += s_scan[w];
       rne += s_scan_ne[w];
     }
-    for (int b = lo; b < hi; ++b) {
-      const int n = s_pre[b + 1];
-      s_ne[b] = (uint16_t)rne;
-      rne += n > 0;
-      run += n;
-      s_pre[b + 1] = run;
+    if (head) {
+      s_ne[b / P] = (uint16_t)(rne - (n > 0));
+      s_pre[b / P + 1] = run;
     }
-    if (tid == kThreads - 1) s_ne[nunits] = (uint16_t)rne;   // the last thread's range ends at nunits
+    if (tid == kThreads - 1) s_ne[nunits] = (uint16_t)rne;
     if (tid == 0) {
       s_pre[0] = 0;
       s_ne[0] = 0;
     }
     __syncthreads();
+  } else {
+    if constexpr (PACK) {
+      // Pages and last-page tokens of every sequence, then each group's prompt pages:
+      // the requested count clamped to the full pages of its shortest member.  The
+      // first requested counts are loaded together with the lengths.
+      const int gs = p.group_size, ngroups = (batch + gs - 1) / gs;
+      const int want0 = tid < ngroups ? p.prefix_pages[tid] : 0;
+      int bad = 0;
+      for (int b = tid; b < batch; b += kThreads) {
+        int L = p.seq_lens[b];
+        if (L < 0 || L > cap) bad = 1;
+        L = min(max(L, 0), cap);
+        const int nf = (L + kPage - 1) / kPage;
+        s_nfull[b] = (uint16_t)nf;
+        s_tail[b] = (uint8_t)(L - (nf - 1) * kPage);
+      }
+      if (bad && u == 0) atomicOr(p.flags, kFlagBadLen);
+      __syncthreads();
+      for (int i = tid; i < ngroups; i += kThreads) {
+        int mn = 0x7fffffff;
+        for (int b = i * gs; b < min(batch, (i + 1) * gs); ++b) {
+          const int nf = s_nfull[b];
+          mn = min(mn, (nf > 0 && s_tail[b] < kPage) ? nf - 1 : nf);   // full pages
+        }
+        const int want = i == tid ? want0 : p.prefix_pages[i], pp = max(0, min(want, mn));
+        if (want != pp && u == 0) atomicOr(p.flags, kFlagPrefixClamped);
+        s_gpp[i] = (int16_t)pp;
+      }
+      __syncthreads();
+    }
+
+    // 1. Page counts per unit and their prefix sums (identical in every workgroup).
+    {
+      const int per = (nunits + kThreads - 1) / kThreads;
+      const int lo = min(tid * per, nunits), hi = min(lo + per, nunits);
+      int sum = 0, cnt = 0, bad = 0;   // pages, non-empty units
+      for (int b = lo; b < hi; ++b) {
+        if constexpr (PACK) {
+          // Pack b: members b0 .. b0 + np - 1 of group i; the prompt once, then each member's own pages.
+          const int gs = p.group_size, P = p.pack, ppg = (gs + P - 1) / P;
+          const int i = b / ppg, r = b - i * ppg;
+          const int b0 = i * gs + r * P, np = min(P, min(batch, (i + 1) * gs) - b0);
+          const int pp = s_gpp[i];
+          int n = pp;
+          for (int m = 0; m < np; ++m) n += s_nfull[b0 + m] - pp;
+          s_ppre[b] = (b0 << 5) | np;
+          s_pre[b + 1] = n;
+          sum += n;
+          cnt += n > 0;
+          continue;
+        }
+        int L = p.seq_lens[b];
+        if (L < 0 || L > cap) bad = 1;
+        L = min(max(L, 0), cap);
+        int nfull = (L + kPage - 1) / kPage;
+        int pp = 0;
+        if constexpr (MULTI) {
+          // Inconsistent offsets, or more rows than the call allows: no rows.  More
+          // rows than tokens: flagged; rows before position 0 see no key (zeros).
+          const int q0 = p.q_start[b], q1 = p.q_start[b + 1];
+          int nq = q1 - q0;
+          if (q0 < 0 || q1 < q0 || q1 > p.total_q || nq > p.max_q_len) {
+            bad = 1;
+            nq = 0;
+          }
+          if (nq > L) bad = 1;
+          if (nq == 0) nfull = 0;
+          s_ppre[b] = nq > 0 ? (q0 << 5) | nq : 0;
+        } else {
+          // Grouped runs: the prompt pass covered the first pp pages (its clamp keeps
+          // pp <= floor(L / 16)); this kernel streams the rest.
+          pp = p.group_size > 0 ? min(max(p.gprefix[b / p.group_size], 0), L / kPage) : 0;
+          s_ppre[b] = pp;
+        }
+        const int n = nfull - pp;
+        s_pre[b + 1] = n;
+        s_tail[b] = (uint8_t)(L - (nfull - 1) * kPage);   // 1..16 when nfull > 0
+        sum += n;
+        cnt += n > 0;
+      }
+      if (bad && u == 0) atomicOr(p.flags, kFlagBadLen);
+      int x = sum, xn = cnt;
+  #pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o), yn = __shfl_up(xn, o);
+        if (lane >= o) {
+          x += y;
+          xn += yn;
+        }
+      }
+      if (lane == 63) {
+        s_scan[wave] = x;
+        s_scan_ne[wave] = xn;
+      }
+      if (tid < p.num_q_heads) s_qhead[tid] = qh0;
+      if (tid < 2 * kWaves) s_seg[tid] = -1;
+      __syncthreads();
+      int run = x - sum, rne = xn - cnt;
+      for (int w = 0; w < wave; ++w) {
+        run += s_scan[w];
+        rne += s_scan_ne[w];
+      }
+      for (int b = lo; b < hi; ++b) {
+        const int n = s_pre[b + 1];
+        s_ne[b] = (uint16_t)rne;
+        rne += n > 0;
+        run += n;
+        s_pre[b + 1] = run;
+      }
+      if (tid == kThreads - 1) s_ne[nunits] = (uint16_t)rne;   // the last thread's range ends at nunits
+      if (tid == 0) {
+        s_pre[0] = 0;
+        s_ne[0] = 0;
+      }
+      __syncthreads();
+    }
   }
   const int64_t T = uni64((int64_t)s_pre[nunits] * Hs);
   // Cost of the flattened list: one per position, and kStartCost more per segment
@@ -1022,7 +1100,7 @@ void decode_attention_kernel(const Params p) {
   //    [floor(u C / Wn), floor((u + 1) C / Wn)), each taken as the positions whose
   //    cost falls inside it.  Each wave walks its own pieces without waiting for
   //    the others; a piece inside its quarter is written directly.
-  int w0, w1;
+  int w0, w1, wunit = 0;   // wunit: the unit of position w0 (when w0 < T)
   int64_t r0, r1;
   {
     // Lane i < 5 turns quarter boundary i into the first position of cost at least
@@ -1044,12 +1122,14 @@ void decode_attention_kernel(const Params p) {
         const int rem = (int)(B - (int64_t)Hs * (pre + S * s_ne[lo]));
         const int gv = rem / (nb + S), q = rem - gv * (nb + S);
         rb = Hs * pre + gv * nb + max(q - S, 0);
+        wunit = lo;
       }
     }
     r0 = __builtin_amdgcn_readfirstlane(rb);
     r1 = __builtin_amdgcn_readlane(rb, kWaves);
     w0 = __builtin_amdgcn_readlane(rb, wave);
     w1 = __builtin_amdgcn_readlane(rb, wave + 1);
+    wunit = __builtin_amdgcn_readlane(wunit, wave);
   }
   // Q operands of the NT tiles, loaded with a segment's first page.
   struct QN {
@@ -1068,12 +1148,14 @@ void decode_attention_kernel(const Params p) {
     // chunk ahead).  The ring runs across chunk boundaries, so it drains only at
     // the end of the quarter.
     const int cn = w1 - w0;   // positions of this quarter (relative index k)
-    auto fetch = [&](int base) {
+    // The unit of a chunk's last position bounds the units of the next chunk from below.
+    auto unit_of_info = [](int info) { return (info >> kInfoSeqShift) & (PACK ? 4095 : 8191); };
+    auto fetch = [&](int base, int hint) {
       return base < w1 ? fetch_chunk<MULTI, PACK>(p, s_pre, s_tail, s_ppre, s_nfull, s_gpp, nunits, base, w0, w1, lane,
-                                                  Hs, nrc)
+                                                  Hs, nrc, hint)
                        : StreamChunk{-1, 0};
     };
-    StreamChunk cur = fetch(w0), nxt = {-1, 0};   // nxt: fetched once the first loads are out
+    StreamChunk cur = fetch(w0, wunit), nxt = {-1, 0};   // nxt: fetched once the first loads are out
     int cbase = 0;   // relative position of cur's first entry
     {
       typename Pol::Frag fr[kDepth];
@@ -1209,13 +1291,14 @@ void decode_attention_kernel(const Params p) {
         if (k + 1 == cbase + kChunk && k + 1 < cn) {
           cur = nxt;
           cbase += kChunk;
-          nxt = fetch(w0 + cbase + kChunk);
+          nxt = fetch(w0 + cbase + kChunk, unit_of_info(__builtin_amdgcn_readlane(cur.info, kChunk - 1)));
         }
       };
 #pragma unroll
       for (int k = 0; k < kDepth - 1; ++k)
         if (k < cn) issue(fr[k], sinfo[k], skm[k], svm[k], qring[k], pring[k], k);
-      nxt = fetch(w0 + kChunk);   // first read kChunk - kDepth + 1 positions from now
+      // First read kChunk - kDepth + 1 positions from now.
+      nxt = fetch(w0 + kChunk, unit_of_info(__builtin_amdgcn_readlane(cur.info, kChunk - 1)));
       int i = 0;
       // Steady state: every position issued lies inside the quarter.
       for (; i + 2 * kDepth - 2 < cn; i += kDepth) {
