@@ -854,7 +854,10 @@ void decode_attention_kernel(const Params p) {
   const int cap = p.max_pages * kPage;
   // Multi-token runs: nrc segments of 16 NT rows per (sequence, KV head), Hs per
   // sequence; a wave holds NT 16-row tiles against each page of a segment.
-  const int nrc = MULTI ? p.row_chunks : 1, Hs = Hkv * nrc;
+  // (Packed grouped runs have one row chunk: a pack's rows fit one segment.)
+  const int nrc = (MULTI && !PACK) ? p.row_chunks : 1, Hs = Hkv * nrc;
+  // Packed grouped runs: the pack member that each of this lane's tile rows belongs to.
+  const int rmem = PACK ? (lane & 15) / G : 0, rmem2 = (PACK && NT == 2) ? (16 + (lane & 15)) / G : 0;
   constexpr int kSegRows = 16 * NT;
   // The 16 NT-row chunk of its (sequence, KV head) that a page's segment covers.
   auto chunk_of_info = [](int info) { return PACK ? 0 : (info >> kInfoChunkShift) & 3; };
@@ -1244,17 +1247,17 @@ void decode_attention_kernel(const Params p) {
         }
         if constexpr (PACK) {
           // A member's own page counts for its rows only; a prompt page for every row.
-          const int act = (info >> kInfoActShift) & 7, tok = info & kInfoTok, r = lane & 15;
+          const int act = (info >> kInfoActShift) & 7, tok = info & kInfoTok;
           // A tile none of whose rows the page serves is skipped (its state would not change).
           if constexpr (NT == 1) {
-            st.template compute<true>(f, lane, (act == kActAll || r / G == act) ? tok : 0, p.scale_log2 * km, vm);
+            st.template compute<true>(f, lane, (act == kActAll || rmem == act) ? tok : 0, p.scale_log2 * km, vm);
           } else {
             const typename Pol::VOp vo = Pol::v_operand(f);
             if (act == kActAll || act * G < 16)
-              st.template compute_with<true>(f, &vo, lane, (act == kActAll || r / G == act) ? tok : 0,
+              st.template compute_with<true>(f, &vo, lane, (act == kActAll || rmem == act) ? tok : 0,
                                              p.scale_log2 * km, vm);
             if (act == kActAll || (act + 1) * G > 16)
-              st2.template compute_with<true>(f, &vo, lane, (act == kActAll || (16 + r) / G == act) ? tok : 0,
+              st2.template compute_with<true>(f, &vo, lane, (act == kActAll || rmem2 == act) ? tok : 0,
                                               p.scale_log2 * km, vm);
           }
         } else if constexpr (MULTI) {
