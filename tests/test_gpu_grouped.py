@@ -214,3 +214,33 @@ def test_packed_path_at_its_largest_batch(torch_cuda):
     got, flags = run_grouped(torch_cuda, w, 8, [2] * (4096 // 8), tag="packed batch 4096")
     assert flags == 0
     assert_close(got, oracle.run(w), "bf16", "packed batch 4096")
+
+
+def test_packed_groups_of_a_whole_wave_with_a_clamped_claim(torch_cuda):
+    # G = 8 (packs of 2), groups of 64 (the largest group whose members fill one wave's
+    # lanes, so the group clamp and the pack sums run as shuffles): two groups, the
+    # second with a member shorter than the claimed prompt, which clamps that group's
+    # prompt and raises flag bit 2.
+    rng = np.random.default_rng(91)
+    tails = rng.integers(0, 300, size=128)
+    tails[::7] = 0
+    w = grouped_case(32, 4, 128, 64, 64, tails.tolist(), seed=92)
+    lens = w.seq_lens.copy()
+    lens[100] = 40   # 2 full pages of the 4-page prompt
+    import dataclasses
+    w = dataclasses.replace(w, seq_lens=lens)
+    got, flags = run_grouped(torch_cuda, w, 64, [4, 4], tag="groups of 64")
+    assert flags == 4
+    assert_close(got, oracle.run(w), "bf16", "groups of 64, clamped")
+
+
+def test_packed_groups_at_one_sequence_per_thread(torch_cuda):
+    # G = 4 (packs of 4), groups of 16, 256 sequences (one per thread of a workgroup,
+    # the lane-aligned prologue's largest batch), with empty members and empty packs.
+    rng = np.random.default_rng(93)
+    tails = rng.integers(0, 200, size=256)
+    tails[rng.choice(256, 60, replace=False)] = 0
+    w = grouped_case(16, 4, 128, 16, 48, tails.tolist(), seed=94)
+    got, flags = run_grouped(torch_cuda, w, 16, [3] * 16, ranges=61, tag="256 sequences, groups of 16")
+    assert flags == 0
+    assert_close(got, oracle.run(w), "bf16", "groups of 16, batch 256")
