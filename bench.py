@@ -128,9 +128,10 @@ def copy_reference(args, torch, dev):
 
 
 def probe_bench(args, torch, dev, w):
-    """Every launch shape of the two read-ceiling probes: the streaming read of a
-    --probe-gib GiB buffer, and the gather of the workload's (K, V) page tiles in the
-    order the decode kernel streams them, over --sets rotated copies of the pools."""
+    """Every launch shape of the read-ceiling probes: the streaming read of a
+    --probe-gib GiB buffer, the gather of the workload's (K, V) page tiles in the
+    order the decode kernel streams them, over --sets rotated copies of the pools, and
+    the same gather with its last tiles claimed in chunks at run time."""
     from paper_2607_09207_amd import accounting as A
     from paper_2607_09207_amd import inputs as I
     from paper_2607_09207_amd import probe
@@ -142,9 +143,12 @@ def probe_bench(args, torch, dev, w):
         sets.append(s)
     sbest, sall = probe.stream_read(torch, dev, gib=args.probe_gib)
     tile = w.page_size * w.head_dim * A.DTYPE_BYTES[w.kv_dtype]
-    gbest, gall = probe.tile_gather(torch, dev, [(s["k_cache"], s["v_cache"]) for s in sets], probe.tile_offsets(w), tile)
+    pools = [(s["k_cache"], s["v_cache"]) for s in sets]
+    gbest, gall = probe.tile_gather(torch, dev, pools, probe.tile_offsets(w), tile)
+    bbest, ball = probe.tile_gather_balanced(torch, dev, pools, probe.tile_offsets(w), tile)
     print(json.dumps({"mode": "probe", "workload": w.name, "tile_bytes": tile, "stream_bytes": int(args.probe_gib * 2**30),
-                      "stream": sall, "gather": gall, "stream_best": sbest, "gather_best": gbest}), flush=True)
+                      "stream": sall, "gather": gall, "gather_balanced": ball, "stream_best": sbest, "gather_best": gbest,
+                      "gather_balanced_best": bbest}), flush=True)
 
 
 def append_bench(args, torch, dev, w, h, ws):

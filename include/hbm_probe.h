@@ -3,7 +3,7 @@
  *
  * The decode-attention path is bound by HBM reads: every call streams each cached
  * KV byte once (the per-token footprint b_kv of App. A.1.2 times the tokens
- * attended).  These two kernels measure what a plain reader reaches on the same
+ * attended).  These kernels measure what a plain reader reaches on the same
  * GPU, so that the attention kernel's rate has a measured ceiling beside the
  * 8 TB/s data-sheet peak.  They do no arithmetic beyond folding the loaded words
  * together, and write (almost) nothing.
@@ -38,6 +38,19 @@ int hbm_probe_stream_read(const void* buf, uint64_t bytes, uint32_t* sink, int b
  * pairs in flight.  `sink` as for hbm_probe_stream_read. */
 int hbm_probe_tile_gather(const void* k_pool, const void* v_pool, const int64_t* tile_offsets, int64_t ntiles,
                           int tile_bytes, uint32_t* sink, int blocks, int threads, int depth, void* stream);
+
+/* The tile gather with run-time balancing: entries [0, nstatic) are cut into equal
+ * contiguous shares, one per wave; the remaining ntiles - nstatic entries (a
+ * multiple of `chunk`, depth <= chunk <= 64) form chunks that waves claim one at a
+ * time with an atomicAdd on counter[0] once their share is done, the load ring
+ * running on across chunks.  `counter` is one 32-bit word of device memory that must
+ * be zero before the first launch; each launch leaves it zero (and launches on one
+ * counter must not overlap).  Shares must hold at least `depth` entries (nstatic /
+ * waves >= depth) or none.  depth 2 to 4; other arguments as for
+ * hbm_probe_tile_gather. */
+int hbm_probe_tile_gather_balanced(const void* k_pool, const void* v_pool, const int64_t* tile_offsets, int64_t ntiles,
+                                   int64_t nstatic, int chunk, uint32_t* counter, int tile_bytes, uint32_t* sink,
+                                   int blocks, int threads, int depth, void* stream);
 
 #ifdef __cplusplus
 }

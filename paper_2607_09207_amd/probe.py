@@ -2,7 +2,8 @@
 
 Two reference readers run on the same GPU as the attention kernel: a contiguous
 streaming read of a large buffer, and a gather of the workload's own (K, V) page
-tiles in the order the decode kernel streams them.  Each is run over a few launch
+tiles in the order the decode kernel streams them.  A third, the same gather with
+its last tiles claimed in chunks at run time, measures what balancing could add.  Each is run over a few launch
 shapes and the best rate is reported; the attention kernel's rate divided by it is
 the fraction of what a plain reader reaches on this GPU.
 """
@@ -29,6 +30,8 @@ def load() -> ctypes.CDLL:
         lib.hbm_probe_stream_read.restype = i32
         lib.hbm_probe_tile_gather.argtypes = [vp, vp, vp, i64, i32, vp, i32, i32, i32, vp]
         lib.hbm_probe_tile_gather.restype = i32
+        lib.hbm_probe_tile_gather_balanced.argtypes = [vp, vp, vp, i64, i64, i32, vp, i32, vp, i32, i32, i32, vp]
+        lib.hbm_probe_tile_gather_balanced.restype = i32
         _lib = lib
     return _lib
 
@@ -117,4 +120,45 @@ def tile_gather(torch, dev, pools, offsets: np.ndarray, tile_bytes: int, reps: i
             res.append({"blocks": blocks, "threads": threads, "depth": depth, "ms": round(ms, 4),
                         "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1)})
     best = max(res, key=lambda r: r["GBps"])
+    return best, res
+
+
+def tile_gather_balanced(torch, dev, pools, offsets: np.ndarray, tile_bytes: int, reps: int = 10, cus: int = 256,
+                         static_fracs=(0.5, 0.75, 0.875, 0.9375), chunks=(8, 16, 32)):
+    """Best rate (GB/s of K and V tile bytes) of the tile gather whose last
+    (1 - static_frac) of the tiles are claimed in chunks at run time, over the
+    static fractions and chunk sizes (one workgroup of 4 waves per CU, ring depth 3).
+    Returns (best, all settings)."""
+    lib = load()
+    off = torch.from_numpy(np.ascontiguousarray(offsets, np.int64)).to(dev)
+    stream = torch.cuda.current_stream(dev)
+    sink = torch.zeros(cus * 64, dtype=torch.int32, device=dev)
+    counter = torch.zeros(64, dtype=torch.int32, device=dev)   # the kernel leaves it zero
+    n = len(offsets)
+    nbytes = 2 * tile_bytes * n
+    blocks, threads, depth = cus, 256, 3
+    waves = blocks * threads // 64
+    res = []
+    for frac in static_fracs:
+        for chunk in chunks:
+            nstatic = n - int(n * (1 - frac)) // chunk * chunk
+            if nstatic // waves < depth:
+                continue
+            it = [0]
+
+            def fn():
+                k_pool, v_pool = pools[it[0] % len(pools)]
+                it[0] += 1
+                st = lib.hbm_probe_tile_gather_balanced(k_pool.data_ptr(), v_pool.data_ptr(), off.data_ptr(), n,
+                                                        nstatic, chunk, counter.data_ptr(), tile_bytes,
+                                                        sink.data_ptr(), blocks, threads, depth, stream.cuda_stream)
+                if st != 0:
+                    raise RuntimeError(f"hbm_probe_tile_gather_balanced: {st}")
+            ms = _time(torch, fn, reps, stream)
+            res.append({"static_frac": frac, "chunk": chunk, "ms": round(ms, 4),
+                        "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1)})
+    torch.cuda.synchronize()
+    if int(counter[0].item()) != 0:
+        raise RuntimeError("balanced gather left its claim counter non-zero")
+    best = max(res, key=lambda r: r["GBps"]) if res else None
     return best, res

@@ -43,7 +43,7 @@ def test_probe_library_exports_its_declared_functions():
     plib = probe.load()
     txt = open(os.path.join(ROOT, "include", "hbm_probe.h")).read()
     names = sorted(set(re.findall(r"^int\s+(hbm_probe_\w+)\s*\(", txt, re.M)))
-    assert names == ["hbm_probe_stream_read", "hbm_probe_tile_gather"]
+    assert names == ["hbm_probe_stream_read", "hbm_probe_tile_gather", "hbm_probe_tile_gather_balanced"]
     for n in names:
         assert hasattr(plib, n), n
     sink = ctypes.c_void_p(256)
@@ -58,6 +58,15 @@ def test_probe_library_exports_its_declared_functions():
                                       sink, 1, 256, 2, None) == -1                             # tile size
     assert plib.hbm_probe_tile_gather(ctypes.c_void_p(256), ctypes.c_void_p(256), ctypes.c_void_p(256), 4, 4096,
                                       sink, 1, 256, 5, None) == -1                             # depth
+    pv = ctypes.c_void_p(256)
+    bal = plib.hbm_probe_tile_gather_balanced
+    assert bal(pv, pv, pv, 64, 0, 16, None, 4096, sink, 1, 256, 3, None) == -1    # no counter
+    assert bal(pv, pv, pv, 64, 0, 2, pv, 4096, sink, 1, 256, 3, None) == -1       # chunk below the depth
+    assert bal(pv, pv, pv, 64, 0, 65, pv, 4096, sink, 1, 256, 3, None) == -1      # chunk above 64
+    assert bal(pv, pv, pv, 64, 10, 16, pv, 4096, sink, 1, 256, 3, None) == -1     # pool not whole chunks
+    assert bal(pv, pv, pv, 64, 8, 8, pv, 4096, sink, 1, 256, 3, None) == -1       # shares of 2 entries < depth
+    assert bal(pv, pv, pv, 64, 80, 16, pv, 4096, sink, 1, 256, 3, None) == -1     # more static entries than tiles
+    assert bal(pv, pv, pv, 64, 0, 16, pv, 4096, sink, 1, 256, 1, None) == -1      # depth
 
 
 def test_tile_offsets_follow_the_stream_order():
