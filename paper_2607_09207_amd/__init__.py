@@ -132,7 +132,11 @@ class DecodeAttention:
             if t.dim() != 4 or tuple(t.shape[1:]) != (cfg.num_kv_heads, cfg.page_size, cfg.head_dim):
                 self._fail(what, f"{name} must be [pages, {cfg.num_kv_heads}, {cfg.page_size}, {cfg.head_dim}], "
                                  f"got {tuple(t.shape)}")
-            if tuple(t.stride()[:3]) != self._kv_strides or t.stride(3) != 1:
+            # A dimension of size 1 is never stepped through, and torch may report any
+            # stride for it (a single KV head of a [page][slot][head][d] cache, a
+            # one-page pool), so only the strides of longer dimensions must match.
+            want = self._kv_strides + (1,)
+            if any(t.stride(i) != want[i] for i in range(4) if t.shape[i] > 1):
                 self._fail(what, f"{name} strides {tuple(t.stride())} differ from the handle's {self._kv_strides} "
                                  "(head_dim contiguous)")
             if t.shape[0] < npages:

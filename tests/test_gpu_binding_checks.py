@@ -4,9 +4,10 @@ handle's configuration, so a mismatch would otherwise read or write out of bound
 import numpy as np
 import pytest
 
+import oracle
 from paper_2607_09207_amd import RldaError
 from paper_2607_09207_amd import inputs as I
-from test_gpu_parity import handle_for
+from test_gpu_parity import assert_close, handle_for
 
 pytestmark = pytest.mark.gpu
 
@@ -70,3 +71,17 @@ def test_fp8_scales_multi_and_append_checks(torch_cuda):
                           v_scale=t["v_scale"])
     assert "v_new" in bad(h.append, kn, kn.float(), k, v, bt, sl, k_scale=t["k_scale"], v_scale=t["v_scale"])
     torch.cuda.synchronize()
+
+
+def test_single_kv_head_in_the_slot_major_layout_is_accepted(torch_cuda):
+    """torch may report any stride for a dimension of size 1 (here the one KV head of a
+    [page][slot][head][d] cache); the binding checks only the strides of longer
+    dimensions, which are the ones the kernels step through."""
+    w = I.to_page_slot_head(I.make_custom([40, 300, 20, 1], 8, 1, 128, seed=17))
+    t = I.to_torch(w, "cuda")
+    h = handle_for(w)
+    out = h(t["q"], t["k_cache"], t["v_cache"], t["block_table"], t["seq_lens"])
+    torch_cuda.cuda.synchronize()
+    assert h.read_flags(device=out.device) == 0
+    assert_close(out.double().cpu().numpy(), oracle.run(w), "bf16", "one KV head, slot-major layout")
+
