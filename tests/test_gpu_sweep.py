@@ -6,13 +6,16 @@ G = Hq / Hkv from 1 to 16 (so tiles with 1 to 15 padding rows), d = 64 and 128, 
 cache dtype, f32 and bf16 output, both cache layouts, shuffled head maps, forced
 work-range counts, and ragged lengths including 0, 1 and page boundaries.  The
 multi-token entry point is swept the same way, on the 128-row kernel and on the
-decode stream (max_q_len).  Every output element is compared.
+decode stream (max_q_len), and the shared-prompt entry point over group sizes,
+prompt lengths, prompt claims and both of its forms.  Every output element is
+compared.
 """
 import numpy as np
 import pytest
 
 import oracle
 from paper_2607_09207_amd import inputs as I
+from test_gpu_grouped import run_grouped
 from test_gpu_multi import run_multi
 from test_gpu_parity import TOL, assert_close, gpu_run, torch_cuda  # noqa: F401  (the fixture)
 
@@ -75,6 +78,26 @@ def _multi_cases(n=16, seed=20260202):
     return out
 
 
+def _grouped_cases(n=16, seed=20260303):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        G = int(rng.integers(1, 17))
+        Hkv = int(rng.choice([1, 2, 4]))
+        kv = str(rng.choice(["bf16", "fp8_e4m3fn"], p=[0.7, 0.3]))
+        d = int(rng.choice([64, 128]))
+        group, ngroups = int(rng.integers(1, 17)), int(rng.integers(1, 4))
+        ptok = 16 * int(rng.integers(1, 33))
+        tails = [int(rng.choice([0, 1, 15, 16, 17])) if rng.random() < 0.4 else int(rng.integers(0, 800))
+                 for _ in range(group * ngroups)]
+        claim = max(0, ptok // 16 - int(rng.choice([0, 0, 1, 3])))   # at most the shared pages: no clamp
+        out.append(dict(i=i, G=G, Hkv=Hkv, kv=kv, d=d, group=group, ngroups=ngroups, ptok=ptok, tails=tails,
+                        claim=claim, hint=int(rng.choice([-1, ptok // 16, 1 << 20])),
+                        strided=bool(rng.random() < 0.25), out=str(rng.choice(["f32", "bf16"])),
+                        ranges=int(rng.choice([0, 7, 29])), seed=int(rng.integers(1, 1 << 30))))
+    return out
+
+
 def _id(c):
     return f"{c['i']}-{c['kv']}-G{c['G']}-Hkv{c['Hkv']}-d{c['d']}"
 
@@ -101,3 +124,18 @@ def test_seeded_multi_token_configurations_match_oracle(torch_cuda, c):
     got, flags = run_multi(torch_cuda, w, out_dtype=c["out"], max_q_len=c["max_q_len"], tag=f"sweep {_id(c)}")
     assert flags == 0
     assert_close(got, oracle.run_multi(w), c["kv"], f"sweep multi {_id(c)}")
+
+
+@pytest.mark.parametrize("c", _grouped_cases(), ids=lambda c: _id(c) + f"-n{c['group']}x{c['ngroups']}-p{c['ptok']}")
+def test_seeded_grouped_configurations_match_oracle(torch_cuda, c):
+    Hq = c["G"] * c["Hkv"]
+    lens = [c["ptok"] + t for t in c["tails"]]
+    w = I.make_custom(lens, Hq, c["Hkv"], c["d"], q_dtype="bf16", kv_dtype=c["kv"], seed=c["seed"],
+                      shared_prefix=(c["group"], c["ptok"]))
+    if c["strided"]:
+        w = I.to_page_slot_head(w)
+    got, flags = run_grouped(torch_cuda, w, c["group"], [c["claim"]] * c["ngroups"], out_dtype=c["out"],
+                             ranges=c["ranges"], hint=c["hint"], tag=f"sweep {_id(c)}")
+    assert flags == 0
+    assert_close(got, oracle.run(w), c["kv"], f"sweep grouped {_id(c)}")
+
