@@ -6,15 +6,17 @@ G = Hq / Hkv from 1 to 16 (so tiles with 1 to 15 padding rows), d = 64 and 128, 
 cache dtype, f32 and bf16 output, both cache layouts, shuffled head maps, forced
 work-range counts, and ragged lengths including 0, 1 and page boundaries.  The
 multi-token entry point is swept the same way, on the 128-row kernel and on the
-decode stream (max_q_len), and the shared-prompt entry point over group sizes,
-prompt lengths, prompt claims and both of its forms.  Every output element is
-compared.
+decode stream (max_q_len), the shared-prompt entry point over group sizes, prompt
+lengths, prompt claims and both of its forms, and the KV append (bit for bit).
+Every output element is compared.
 """
 import numpy as np
 import pytest
 
 import oracle
 from paper_2607_09207_amd import inputs as I
+from oracle import append as OA
+from test_gpu_append import assert_same, gpu_append, new_rows
 from test_gpu_grouped import run_grouped
 from test_gpu_multi import run_multi
 from test_gpu_parity import TOL, assert_close, gpu_run, torch_cuda  # noqa: F401  (the fixture)
@@ -98,6 +100,21 @@ def _grouped_cases(n=16, seed=20260303):
     return out
 
 
+def _append_cases(n=16, seed=20260404):
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        kv = str(rng.choice(["f32", "bf16", "fp8_e4m3fn"], p=[0.2, 0.4, 0.4]))
+        B = int(rng.integers(1, 10))
+        G, d = int(rng.integers(1, 5)), int(rng.choice([64, 128]))
+        if kv == "f32":                                      # fp32 handles hold G * d <= 128
+            G, d = 1 + (G - 1) % 2, 64
+        out.append(dict(i=i, G=G, Hkv=int(rng.choice([1, 2, 4, 8])), kv=kv, d=d, lens=_lengths(rng, B, 1200),
+                        mags=(10.0 ** rng.uniform(-2, 2, B)).tolist(), strided=bool(rng.random() < 0.3),
+                        seed=int(rng.integers(1, 1 << 30))))
+    return out
+
+
 def _id(c):
     return f"{c['i']}-{c['kv']}-G{c['G']}-Hkv{c['Hkv']}-d{c['d']}"
 
@@ -138,4 +155,17 @@ def test_seeded_grouped_configurations_match_oracle(torch_cuda, c):
                              ranges=c["ranges"], hint=c["hint"], tag=f"sweep {_id(c)}")
     assert flags == 0
     assert_close(got, oracle.run(w), c["kv"], f"sweep grouped {_id(c)}")
+
+
+@pytest.mark.parametrize("c", _append_cases(), ids=_id)
+def test_seeded_append_configurations_are_bit_exact(torch_cuda, c):
+    Hq = c["G"] * c["Hkv"]
+    w = I.make_custom(c["lens"], Hq, c["Hkv"], c["d"], q_dtype="f32" if c["kv"] == "f32" else "bf16",
+                      kv_dtype=c["kv"], seed=c["seed"])
+    if c["strided"]:
+        w = I.to_page_slot_head(w)
+    kn, vn = new_rows(w, np.random.default_rng(c["seed"] + 1), mags=c["mags"])
+    got = gpu_append(torch_cuda, w, kn, vn)
+    assert got[4] == 0
+    assert_same(got[:4], OA.append(w, kn, vn), f"sweep append {_id(c)} lens={c['lens']}")
 
