@@ -13,6 +13,7 @@ import pytest
 import oracle
 from paper_2607_09207_amd import inputs as I
 from test_gpu_parity import assert_close, handle_for, log
+from test_gpu_sweep import KV_OF_Q, _decode_cases, _head_map, _id
 
 pytestmark = pytest.mark.gpu
 
@@ -77,3 +78,21 @@ def test_noalloc_rejects_batches_beyond_its_scratch(torch_cuda):
     with pytest.raises(RldaError) as e:
         h.run_noalloc(q, t["k_cache"], t["v_cache"], bt, sl)
     assert e.value.status == -6
+
+
+@pytest.mark.parametrize("c", _decode_cases(), ids=_id)
+def test_noalloc_equals_the_workspace_call_over_the_seeded_sweep(torch_cuda, c):
+    """The seeded decode configurations, one after another on the one static array:
+    each no-allocation call equals the workspace call bit for bit."""
+    Hq = c["G"] * c["Hkv"]
+    rng = np.random.default_rng(c["seed"])
+    w = I.make_custom(c["lens"], Hq, c["Hkv"], c["d"], q_dtype=KV_OF_Q[c["kv"]], kv_dtype=c["kv"], seed=c["seed"],
+                      extra_pages=2, kv_head_of_q=_head_map(rng, Hq, c["Hkv"], c["shuffle"]))
+    if c["strided"]:
+        w = I.to_page_slot_head(w)
+    log(f"noalloc sweep {_id(c)} lens={c['lens']} out={c['out']} ranges={c['ranges']}")
+    h = handle_for(w, c["out"], c["ranges"])
+    got, ref, flags = both(torch_cuda, h, w)
+    assert flags == 0
+    assert torch_cuda.equal(got, ref), f"{_id(c)}: differs from rl_decode_attn_run"
+
