@@ -15,10 +15,10 @@
 // GPU fill longest-job-first.
 //
 // Keys.  The workgroup walks its causal key range in blocks of 32 keys (two
-// pages).  Each wave brings one page of K or V of every block, two blocks ahead
-// (page ids come through the scalar cache one block before that): bf16 pages at
-// d = 128 by buffer-load DMA straight into LDS, other caches through registers
-// (fp8 converted exactly to bf16 on the way).  Per block:
+// pages).  Each wave brings one page of K or V of every block (page ids come
+// through the scalar cache one block before that): bf16 pages at d = 128 by
+// buffer-load DMA straight into LDS, two blocks ahead; other caches through
+// registers one block ahead (fp8 converted exactly to bf16 on the way).  Per block:
 //   S^T[key][row] = K Q^T    v_mfma_f32_32x32x16_bf16, K from LDS, Q in registers;
 //   online softmax per row (lanes l and l^32 hold one row), with the reference
 //   maximum moved only when a score exceeds it by more than 2^8;
@@ -54,8 +54,11 @@ constexpr int kNT = kMultiTiles;              // 32-row tiles per wave
 constexpr int kKH = RLDA_MQ_KEY_TILES;
 constexpr int kKeys = kTile * kKH;            // keys per block (2 kKH pages)
 
+#ifndef RLDA_MQ_WAVES_D64
+#define RLDA_MQ_WAVES_D64 4                   // waves per SIMD at d = 64 (about 100 registers)
+#endif
 #ifndef RLDA_MQ_PREFETCH
-#define RLDA_MQ_PREFETCH 2                    // blocks loaded ahead into registers (register staging)
+#define RLDA_MQ_PREFETCH 1                    // blocks loaded ahead into registers (register staging)
 #endif
 #ifndef RLDA_MQ_DMA
 #define RLDA_MQ_DMA 1                         // bf16, d = 128: pages go to LDS by buffer-load DMA
@@ -84,16 +87,15 @@ struct MqShape {
   // (fp8 is converted on the way) into padded rows.
   static constexpr bool DMA = !FP8 && D == 128 && RLDA_MQ_DMA;
   static constexpr int NBUF = DMA ? 3 : 2;    // LDS block buffers
-  // Waves per SIMD (register budget 512 / waves).  Without staging registers the
-  // DMA path fits three (167 registers) when the V operands are read after the
-  // softmax; the register path keeps two and reads V before the softmax, where
-  // the read latency overlaps it.
+  // Waves per SIMD (register budget 512 / waves).  With the V operands read after
+  // the softmax, three fit (168 registers): the DMA path without staging registers,
+  // the register path with one block of staging in flight.  At d = 64 the state is
+  // about 100 registers, and four fit.
 #ifdef RLDA_MQ_WAVES
   static constexpr int WAVES = RLDA_MQ_WAVES;
 #else
-  static constexpr int WAVES = kNT == 1 ? (DMA ? 3 : 2) : 1;
+  static constexpr int WAVES = kNT == 1 ? (D == 64 ? RLDA_MQ_WAVES_D64 : 3) : 1;
 #endif
-  static constexpr bool V_EARLY = !DMA;
   static constexpr int KRS = DMA ? 2 * D : 2 * D + RLDA_MQ_KPAD;   // LDS row stride of the K block (bytes)
   static constexpr int VRS = DMA ? 2 * D : 2 * D + RLDA_MQ_VPAD;   // ... of the V block
   static constexpr int CPR = D * EB / 16;     // 16-byte chunks per cached row
@@ -605,11 +607,10 @@ void multi_query_kernel(const Params p) {
           for (int t = 0; t < kNT; ++t)
             sc[t][kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[s], qop[t][s], sc[t][kh], 0, 0, 0);
       }
-      if constexpr (S::V_EARLY) read_v(va[0], buf, 0);   // its latency overlaps the softmax
 #pragma unroll
       for (int t = 0; t < kNT; ++t) softmax(t, kb, buf, sc[t]);
 #pragma unroll
-      for (int kh = S::V_EARLY ? 1 : 0; kh < kKH; ++kh) read_v(va[kh], buf, kh);
+      for (int kh = 0; kh < kKH; ++kh) read_v(va[kh], buf, kh);
 #pragma unroll
       for (int kh = 0; kh < kKH; ++kh)
 #pragma unroll
