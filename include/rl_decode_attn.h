@@ -152,7 +152,8 @@ rlda_status rl_decode_attn_run_profiled(rl_decode_attn_t handle, int32_t batch, 
  *     on, held until the process ends), found on the first call on each device;
  *   - limits of that array: batch * num_kv_heads <= 65536 and head_dim <= 128
  *     (else RLDA_ERR_SCRATCH, nothing launched), and the work is cut into at most
- *     512 shares (the default: one per CU on MI355X, two for fp8 caches);
+ *     512 shares (the default: one per CU on MI355X, two for fp8 caches and
+ *     for bf16 caches at head_dim 64);
  *   - flags: NULL, or a caller-owned device uint32_t (4-byte aligned) that receives
  *     the contract bits of rl_decode_attn_read_flags (OR-ed in; the caller clears
  *     it).  With NULL they go to a word of the static array that nothing reads.

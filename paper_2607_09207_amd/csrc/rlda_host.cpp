@@ -225,10 +225,12 @@ rlda_status run_impl(rl_decode_attn_t h, int32_t batch, int32_t num_pages, int32
   if (hipGetDevice(&dev) != hipSuccess) return RLDA_ERR_HIP;
   // One workgroup (one wave per SIMD) per CU by default: a second workgroup on a
   // CU would lose instruction arbitration to the first and finish its share later.
-  // fp8 pages are half the bytes of bf16 ones, and four waves per CU cannot keep
-  // enough of them in flight: plain fp8 runs of up to kTwoWgMaxBatch sequences take
-  // two workgroups per CU (two waves per SIMD, within 256 registers each).
-  const bool two = !grouped && h->kind == rlda::KvKind::FP8 && batch <= rlda::kTwoWgMaxBatch;
+  // fp8 pages, and bf16 pages at d = 64, are half the bytes of bf16 ones at d = 128,
+  // and four waves per CU cannot keep enough of them in flight: such plain runs of
+  // up to kTwoWgMaxBatch sequences take two workgroups per CU (two waves per SIMD,
+  // within 256 registers each).
+  const bool half_pages = h->kind == rlda::KvKind::FP8 || (h->kind == rlda::KvKind::BF16 && c.head_dim == 64);
+  const bool two = !grouped && half_pages && batch <= rlda::kTwoWgMaxBatch;
   int ranges = c.num_work_ranges;
   if (ranges == 0) {
     ranges = cu_count(dev);

@@ -1850,6 +1850,8 @@ int launch_decode_packed(KvKind kind, int head_dim, int tiles, const Params& p, 
 }
 
 int launch_decode_two(KvKind kind, int head_dim, const Params& p, void* stream, void* ev_begin, void* ev_end) {
+  if (kind == KvKind::BF16)
+    return head_dim == 64 ? launch<Mfma<64, false>, false, 1, false, false, 2>(p, stream, ev_begin, ev_end) : -1;
   if (kind != KvKind::FP8) return -1;
   return head_dim == 128 ? launch<Mfma<128, true>, false, 1, false, false, 2>(p, stream, ev_begin, ev_end)
                          : launch<Mfma<64, true>, false, 1, false, false, 2>(p, stream, ev_begin, ev_end);

@@ -102,8 +102,9 @@ int launch_decode(KvKind kind, int head_dim, int group, const Params& p, void* s
 // followed by the attention kernel.
 int launch_grouped(KvKind kind, int head_dim, int group, const Params& p, int ngroups, void* stream,
                    void* ev_begin, void* ev_end);
-// fp8 decode with two workgroups per CU (two waves per SIMD; batch <= kTwoWgMaxBatch,
-// nranges twice the CUs): eight waves per CU keep twice the 2 KiB tiles in flight.
+// Decode with two workgroups per CU for the half-size pages (fp8, and bf16 at d = 64;
+// two waves per SIMD; batch <= kTwoWgMaxBatch, nranges twice the CUs): eight waves
+// per CU keep twice the tiles in flight.
 int launch_decode_two(KvKind kind, int head_dim, const Params& p, void* stream, void* ev_begin, void* ev_end);
 // KV append: one wave per (sequence, KV head).
 int launch_append(KvKind kind, int head_dim, const Params& p, void* stream);
@@ -130,7 +131,7 @@ constexpr int kMultiMaxBatch = 4096;   // its per-sequence LDS tables stay withi
 constexpr int kPackMaxBatch = 4096;    // packed grouped runs: per-sequence and per-pack LDS tables of this size
 constexpr int kPackMaxMembers = 7;     // ... members per pack (3 bits of the page descriptor, 7 = every member)
 constexpr int kPackMaxPages = 32767;   // ... pages per sequence (16-bit LDS entries)
-constexpr int kTwoWgMaxBatch = 512;      // two workgroups per CU (fp8 decode): per-sequence LDS tables of this size
+constexpr int kTwoWgMaxBatch = 512;      // two workgroups per CU (fp8, bf16 d = 64 decode): per-sequence LDS tables of this size
 constexpr int kTwoTileMaxBatch = 2048;   // two-tile multi-token rows: per-sequence LDS tables of this size
                                          // leave room for 32-row merge slots
 

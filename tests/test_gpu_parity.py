@@ -352,19 +352,20 @@ def test_split_merge_handoff_under_repetition(torch_cuda):
     assert bad == 0
 
 
+@pytest.mark.parametrize("kv,d", [("fp8_e4m3fn", 128), ("bf16", 64)])
 @pytest.mark.parametrize("batch", [512, 513])
-def test_fp8_on_either_side_of_the_two_workgroup_limit(torch_cuda, batch):
-    """Plain fp8 runs of up to 512 sequences take two workgroups per CU (two waves per
-    SIMD); larger batches one.  Both against the oracle, at the default work split and
-    a forced one."""
+def test_half_size_pages_on_either_side_of_the_two_workgroup_limit(torch_cuda, batch, kv, d):
+    """Plain runs over half-size pages (fp8 at d = 128, bf16 at d = 64) of up to 512
+    sequences take two workgroups per CU (two waves per SIMD); larger batches one.
+    Both against the oracle, at the default work split and a forced one."""
     rng = np.random.default_rng(90 + batch)
     lens = rng.integers(0, 300, size=batch)
     lens[rng.choice(batch, size=6, replace=False)] = rng.integers(2000, 6000, size=6)
-    w = I.make_custom(lens.tolist(), 40, 8, 128, q_dtype="bf16", kv_dtype="fp8_e4m3fn", seed=91)
+    w = I.make_custom(lens.tolist(), 40, 8, d, q_dtype="bf16", kv_dtype=kv, seed=91)
     for ranges in (0, 333):
-        got, flags = gpu_run(torch_cuda, w, ranges=ranges, tag=f"fp8 batch {batch} ranges={ranges}")
+        got, flags = gpu_run(torch_cuda, w, ranges=ranges, tag=f"{kv} d={d} batch {batch} ranges={ranges}")
         assert flags == 0
-        assert_close(got, oracle.run(w), "fp8_e4m3fn", f"fp8 batch {batch} ranges={ranges}")
+        assert_close(got, oracle.run(w), kv, f"{kv} d={d} batch {batch} ranges={ranges}")
 
 
 def test_maximum_batch(torch_cuda):
