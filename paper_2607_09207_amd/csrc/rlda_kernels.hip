@@ -1392,40 +1392,36 @@ void decode_attention_kernel(const Params p) {
       }
       if (!whole && nhand < 2) hand_seg[nhand++] = cur;   // only the first and last group can be cut
     };
-    // Slots in position order; the used slots of one segment are consecutive.  The
-    // LDS reads of slot j + 1 (max/sum, partial output) are issued before slot j is
-    // merged, so their latency overlaps the merge and the stores.
-    float mn, ln, vn[DPT];
-    auto load_slot = [&](int j) {
-      mn = s_ml[j][h][0];
-      ln = s_ml[j][h][1];
+    // Slots in position order; the used slots of one segment are consecutive.  Every
+    // slot's max/sum and partial output, and this thread's output head for every
+    // slot's segment, are read from LDS before the first merge (unused slots read
+    // values that are never used), so the merge waits for LDS once, not per slot.
+    float ms[2 * kWaves], ls[2 * kWaves], vs[2 * kWaves][DPT];
+    int qhs[2 * kWaves];
 #pragma unroll
-      for (int c = 0; c < DPT; c += 4) *(f32x4*)&vn[c] = *(const f32x4*)&s_acc[j][h][d0 + c];
-    };
-    load_slot(0);
-#pragma unroll 1
+    for (int j = 0; j < 2 * kWaves; ++j) {
+      ms[j] = s_ml[j][h][0];
+      ls[j] = s_ml[j][h][1];
+#pragma unroll
+      for (int c = 0; c < DPT; c += 4) *(f32x4*)&vs[j][c] = *(const f32x4*)&s_acc[j][h][d0 + c];
+      qhs[j] = out_head(__builtin_amdgcn_readlane(lg, j));
+    }
+#pragma unroll
     for (int j = 0; j <= 2 * kWaves; ++j) {
-      int sj = -2;   // -2: past the last slot
-      float mj = mn, lj = ln, v[DPT];
-#pragma unroll
-      for (int e = 0; e < DPT; ++e) v[e] = vn[e];
-      if (j < 2 * kWaves) {
-        sj = __builtin_amdgcn_readlane(lseg, j);
-        if (j + 1 < 2 * kWaves) load_slot(j + 1);
-      }
+      const int sj = j < 2 * kWaves ? __builtin_amdgcn_readlane(lseg, j) : -2;   // -2: past the last slot
       if (sj == -1) continue;   // unused slot
       if (sj != cur) {
         if (cur >= 0) flush();
         cur = sj;
         jcur = j;
-        if (sj >= 0) qh_cur = out_head(__builtin_amdgcn_readlane(lg, j));
+        if (sj >= 0) qh_cur = qhs[j];
         M = neg_inf();
         Ls = 0.f;
 #pragma unroll
         for (int e = 0; e < DPT; ++e) o[e] = 0.f;
       }
       if (sj >= 0 && h < seg_rows(__builtin_amdgcn_readlane(lb, j), __builtin_amdgcn_readlane(lg, j)))
-        lse_merge<DPT>(M, Ls, o, mj, lj, v);
+        lse_merge<DPT>(M, Ls, o, ms[j], ls[j], vs[j]);
     }
   }
 
